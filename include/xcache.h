@@ -1,0 +1,226 @@
+/*
+ * xcache.h -- C ABI of the MI355X (gfx950) X-Cache cached chunk forward.
+ *
+ * The library runs the causal multi-block DiT forward of one few-step
+ * generation chunk under X-Cache's cross-chunk block cache:
+ *
+ *   - rollout structure (Section 2.1, Eq. 1-2): generation n, denoising step
+ *     t in [0, S), blocks b in [0, B); x_{t,b} = x_{t,b-1} + f_b(x_{t,b-1}; c_t);
+ *     after the S steps one extra KV-update pass on the clean latent writes the
+ *     chunk's keys/values into a rolling FIFO cache;
+ *   - per-(t, b) residual cache and additive reuse (Section 2.2, Eq. 3-4);
+ *   - fingerprint of each block input: a 3-D grid subsample per view group,
+ *     a per-camera token-mean global channel and the chunk's action vector
+ *     (Section 2.3.1-2.3.2);
+ *   - dual-metric gate: min-cosine over all fingerprint entries, max token
+ *     deviation over the spatial group entries, skip iff both pass
+ *     (Section 2.3.3-2.3.5, Eq. 5-7);
+ *   - adaptive per-(t, b) cosine threshold from an EMA (Section 2.4, Eq. 8-9);
+ *   - safety mechanisms (Section 2.5): step-0 protection, front/back anchor
+ *     blocks, KV-update protection (always on), maximum staleness.
+ *
+ * Conventions for every entry point:
+ *   - Device pointers are HIP device addresses on the device that was current
+ *     at xc_init; host pointers are ordinary CPU memory.  The caller owns every
+ *     buffer it passes; the library owns everything it allocates.
+ *   - All arguments are validated before anything is enqueued; a call that
+ *     returns an error has changed no state, with the exception of
+ *     XC_ERR_HIP, which is sticky: the handle must then be destroyed.
+ *   - Work is enqueued on the stream bound at xc_init and the call returns
+ *     without synchronising, except xc_stats and xc_kernel_times, which
+ *     synchronise that stream.
+ *   - A handle is not thread-safe; calls on one handle must be serialised.
+ *   - No C++ exception crosses this ABI.
+ */
+#ifndef XCACHE_H
+#define XCACHE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum xc_status {
+  XC_OK = 0,
+  XC_ERR_INVALID_ARG = 1,  /* a pointer, size or configuration field is invalid */
+  XC_ERR_STATE = 2,        /* call not allowed in the handle's current state     */
+  XC_ERR_OOM = 3,          /* device or host allocation failed                  */
+  XC_ERR_HIP = 4,          /* a HIP runtime call failed (sticky)                 */
+  XC_ERR_UNSUPPORTED = 5   /* valid request this build does not implement        */
+} xc_status;
+
+/* model dtype: the residual stream is always float32; XC_BF16 stores weights,
+ * activations, the KV cache and cached residuals in bf16 and runs the
+ * contractions on bf16 matrix cores with float32 accumulation. */
+enum { XC_F32 = 0, XC_BF16 = 1 };
+enum { XC_STEP0_OFF = 0, XC_STEP0_FORCE = 1, XC_STEP0_STRICT = 2 };
+enum { XC_FP_GRID3D = 0, XC_FP_LINSPACE1D = 1 };
+/* xc_forward_chunk flags */
+enum { XC_FORCE_FULL = 1u };
+/* per-block decision codes reported by xc_stats for the last denoising pass */
+enum { XC_DEC_COMPUTE = 0, XC_DEC_SKIP = 1, XC_DEC_FORCED = 2, XC_DEC_NONE = 255 };
+
+#define XC_MAX_GROUPS 8
+#define XC_MAX_COND 512   /* temb_dim + action_dim */
+#define XC_MAX_ACTION 64
+
+/* Cameras sharing one latent grid (a view group, Section 2.3.1). */
+typedef struct xc_view_group {
+  int32_t views;   /* cameras stacked along V                         */
+  int32_t frames;  /* latent frames per chunk (F)                      */
+  int32_t height;  /* latent rows (H)                                  */
+  int32_t width;   /* latent columns (W)                               */
+} xc_view_group;
+
+/* Model shape.  Tokens L = sum over groups of views*frames*height*width,
+ * camera-major, each camera's (f, h, w) grid row-major.
+ * Constraints: hidden == n_heads * head_dim; temb_dim even;
+ * temb_dim + action_dim <= XC_MAX_COND; action_dim <= XC_MAX_ACTION;
+ * XC_BF16 additionally needs head_dim in {64, 128} and hidden, mlp_hidden
+ * multiples of 128.  Block internals: LayerNorm without affine (eps 1e-6),
+ * six-way adaLN modulation from W_ada SiLU(c) + b_ada with
+ * c = [sinusoidal temb(timestep); action], QK RMSNorm (eps 1e-6) with gains,
+ * softmax attention over the rolling cache (no mask), tanh-GELU MLP. */
+typedef struct xc_model_config {
+  int32_t n_blocks;    /* B                                                */
+  int32_t hidden;      /* C                                                */
+  int32_t n_heads;     /* H                                                */
+  int32_t head_dim;    /* d                                                */
+  int32_t mlp_hidden;  /* D_m                                              */
+  int32_t temb_dim;    /* D_t                                              */
+  int32_t action_dim;  /* A                                                */
+  int32_t dtype;       /* XC_F32 or XC_BF16                                */
+  int32_t n_steps;     /* S denoising steps per chunk                      */
+  int32_t kv_window;   /* chunks visible to attention, current included    */
+  int32_t n_groups;    /* 1..XC_MAX_GROUPS                                 */
+  xc_view_group groups[XC_MAX_GROUPS];
+} xc_model_config;
+
+/* Gate hyper-parameters; names and defaults follow Table 1. */
+typedef struct xc_gate_config {
+  int32_t enabled;        /* 0: plain DiT, no fingerprints, no cache          */
+  int32_t fp_budget;      /* K tokens per camera fingerprint (32)             */
+  int32_t warmup;         /* W >= 1 generations computed in full (1)          */
+  int32_t front_anchors;  /* F_n always-computed leading blocks (1)           */
+  int32_t back_anchors;   /* B_n always-computed trailing blocks (0)          */
+  int32_t adaptive;       /* 1: EMA threshold (Eq. 8-9); 0: tau_cos_fixed     */
+  float tau_floor;        /* quality floor (0.97)                             */
+  float margin;           /* m (0.02)                                         */
+  float alpha;            /* EMA coefficient in [0, 1] (0.3)                  */
+  float tau_cos_fixed;    /* cosine threshold when adaptive == 0              */
+  float tau_dev;          /* deviation threshold (2.0); +inf allowed          */
+  float eps;              /* epsilon of Eq. 6 (1e-6)                          */
+  int32_t max_stale;      /* M consecutive skips allowed, 0 = off             */
+  int32_t step0_mode;     /* XC_STEP0_OFF / _FORCE / _STRICT                  */
+  float tau_strict0;      /* strict step-0 threshold (0.999)                  */
+  int32_t kv_protect;     /* must be 1: KV-update passes are never gated      */
+  int32_t fp_mode;        /* XC_FP_GRID3D or XC_FP_LINSPACE1D                 */
+} xc_gate_config;
+
+typedef struct xc_stats_t {
+  int64_t generations;        /* completed KV-update passes (n)                  */
+  int64_t evals_post_warmup;  /* B per denoising pass with n >= W                */
+  int64_t gated_evals;        /* (t, b) gate tests actually evaluated            */
+  int64_t skips;              /* block evaluations that reused a residual        */
+  int64_t kv_block_evals;     /* B per KV-update pass                            */
+  int32_t last_step;          /* t of the last pass, S for KV-update, -1 none    */
+} xc_stats_t;
+
+typedef struct xc_handle xc_handle;
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* xc_status_string(xc_status s);
+
+/* Create a handle (Section 2.1 state: weights, rolling KV cache, residual and
+ * fingerprint caches, EMA and staleness tables).
+ *   model, gate     : host structs, copied.
+ *   weights_host    : host float32 blob, per block in this order, row-major
+ *                     [out, in]: W_ada [6C, D_t+A], b_ada [6C], Wq [C, C], bq,
+ *                     Wk [C, C], bk, Wv [C, C], bv, Wo [C, C], bo,
+ *                     W1 [D_m, C], b1, W2 [C, D_m], b2, gq [d], gk [d];
+ *                     blocks concatenated.  Copied (converted to bf16 for
+ *                     XC_BF16) before return; the caller may free it.
+ *   weights_bytes   : must equal 4 * the blob's element count.
+ *   hip_stream      : hipStream_t all work is enqueued on (NULL = default).
+ *   out             : receives the handle.
+ * Errors: XC_ERR_INVALID_ARG (NULL pointers, bad shape or gate field, size
+ * mismatch), XC_ERR_UNSUPPORTED (kv_protect == 0, unsupported head_dim),
+ * XC_ERR_OOM, XC_ERR_HIP.  Synchronises the stream once (weight upload). */
+xc_status xc_init(const xc_model_config* model, const xc_gate_config* gate,
+                  const float* weights_host, size_t weights_bytes, void* hip_stream,
+                  xc_handle** out);
+
+/* One denoising pass (step t) of the current generation n (Eq. 1) under the
+ * cross-chunk gate (Eq. 3-9, Section 2.5).
+ *   step        : t in [0, S).
+ *   timestep    : the diffusion timestep fed to the sinusoidal embedding.
+ *   action_host : host float32 [action_dim], the chunk's action vector.
+ *   x_in        : device float32 [L, C], the latent entering block 0.
+ *   x_out       : device float32 [L, C], receives the last block's output;
+ *                 may alias x_in.
+ *   flags       : XC_FORCE_FULL computes every block but still refreshes the
+ *                 fingerprint and residual caches (KV-update generation
+ *                 protection, Section 2.5 item 3).
+ * The current chunk's keys/values of each computed block are written into
+ * this generation's cache slot and attended together with the kept past
+ * chunks; they are replaced by the clean ones at xc_kv_update.
+ * Decisions stay on the device; nothing is copied back. */
+xc_status xc_forward_chunk(xc_handle* h, int32_t step, float timestep, const float* action_host,
+                           const void* x_in, void* x_out, uint32_t flags);
+
+/* The KV-update pass (Section 2.1; protection of Section 2.5 item 3): every
+ * block computed in full on the clean latent, its keys/values committed to
+ * the generation's slot of the rolling cache (the oldest chunk is evicted once
+ * kv_window - 1 past chunks are kept), the action remembered for the next
+ * generation's action channel, then n <- n + 1.  Never gated.
+ *   x_clean : device float32 [L, C].
+ *   x_out   : device float32 [L, C] or NULL (output not needed). */
+xc_status xc_kv_update(xc_handle* h, float timestep, const float* action_host,
+                       const void* x_clean, void* x_out);
+
+/* Synchronise the stream and copy out counters and per-(t, b) state.
+ * Every array pointer may be NULL.  skip_counts: int32 [S * B] (t-major);
+ * last_decision: uint8 [B] for the last denoising pass (XC_DEC_*;
+ * XC_DEC_NONE before any); last_cos, last_dev, last_tau: float [B] (NaN where
+ * the gate was not evaluated); ema: float [S * B] (NaN where unset). */
+xc_status xc_stats(xc_handle* h, xc_stats_t* stats, int32_t* skip_counts, uint8_t* last_decision,
+                   float* last_cos, float* last_dev, float* last_tau, float* ema);
+
+/* Start a new rollout: clears the KV cache, residual/fingerprint caches, EMA,
+ * staleness and counters; keeps the weights. */
+xc_status xc_reset(xc_handle* h);
+
+/* Release everything the handle owns (synchronises its stream).  NULL is a
+ * no-op. */
+xc_status xc_destroy(xc_handle* h);
+
+/* Sampler helper for the rollout driver: out = a*x + b*y over n float32
+ * device elements (out may alias x or y). */
+xc_status xc_axpby(xc_handle* h, float a, const void* x, float b, const void* y, void* out, size_t n);
+
+/* Host-only (no HIP call): the token rows the fingerprint samples, per view
+ * group in order, camera by camera (Section 2.3.1).  Writes up to cap int32
+ * global row indices into rows (may be NULL) and the total into *n_rows. */
+xc_status xc_fingerprint_rows(const xc_model_config* model, const xc_gate_config* gate,
+                              int32_t* rows, size_t cap, size_t* n_rows);
+
+/* Kernel timing: while enabled, every launch of the kernel kinds below is
+ * bracketed by HIP events on the bound stream. */
+enum {
+  XC_KERN_ATTENTION = 0, XC_KERN_GEMM_QKV = 1, XC_KERN_GEMM_OPROJ = 2, XC_KERN_GEMM_UP = 3,
+  XC_KERN_GEMM_DOWN = 4, XC_KERN_GATE_REDUCE = 5, XC_KERN_GATE_COMPARE = 6, XC_KERN_GATE_DECIDE = 7,
+  XC_KERN_SKIP_ADD = 8, XC_KERN_LN_MOD = 9, XC_KERN_QK_NORM = 10, XC_KERN_ADALN = 11,
+  XC_KERN_COUNT = 12
+};
+xc_status xc_profile(xc_handle* h, int32_t enable);
+
+/* Synchronise, then report launches and summed event time (ms) of one kernel
+ * kind since profiling was enabled or last cleared; clear != 0 resets it. */
+xc_status xc_kernel_times(xc_handle* h, int32_t kind, int64_t* launches, double* total_ms, int32_t clear);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* XCACHE_H */

@@ -1,0 +1,299 @@
+// HBM-bound kernels of the block: conditioning, adaLN modulation GEMV,
+// LayerNorm + modulation, QK RMSNorm with the scatter into the KV cache,
+// the cached-residual add of a skipped block and the sampler axpby.
+//
+// Every kernel that belongs to a block's compute path takes `flag`: when it is
+// non-null and the block's skip flag is set, the kernel returns at entry
+// (wave-uniformly), so a skipped block costs one empty launch.
+#include "xc_internal.h"
+
+#include <math.h>
+
+namespace xc {
+
+namespace {
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+template <typename T>
+__device__ __forceinline__ T to_t(float v);
+template <>
+__device__ __forceinline__ float to_t<float>(float v) { return v; }
+template <>
+__device__ __forceinline__ bf16 to_t<bf16>(float v) { return (bf16)v; }
+
+__device__ __forceinline__ float to_f(float v) { return v; }
+__device__ __forceinline__ float to_f(bf16 v) { return (float)v; }
+
+// c = [temb(timestep); action]; cond_silu = SiLU(c).  temb is the sinusoidal
+// embedding [cos(tau f_i), sin(tau f_i)], f_i = 10000^(-i/h), h = temb_dim/2,
+// evaluated in double so the large arguments (tau up to 1000) keep full
+// float accuracy.
+struct CondArgs {
+  float action[kMaxAction];
+};
+
+__global__ void cond_kernel(CondArgs a, int temb_dim, int action_dim, float timestep, float* cond_silu) {
+  const int h = temb_dim / 2;
+  for (int j = threadIdx.x; j < temb_dim + action_dim; j += blockDim.x) {
+    double c;
+    if (j < h) {
+      c = cos((double)timestep * exp(-log(10000.0) * (double)j / (double)h));
+    } else if (j < temb_dim) {
+      c = sin((double)timestep * exp(-log(10000.0) * (double)(j - h) / (double)h));
+    } else {
+      c = (double)a.action[j - temb_dim];
+    }
+    cond_silu[j] = (float)(c / (1.0 + exp(-c)));
+  }
+}
+
+// mod[blk][r] = sum_j W_ada[blk][r][j] * cond_silu[j] + b_ada[blk][r]: one wave
+// per output row, lanes striding the conditioning vector (coalesced rows).
+template <typename T>
+__global__ __launch_bounds__(256) void adaln_kernel(const T* __restrict__ w, const float* __restrict__ b,
+                                                    const float* __restrict__ cond_silu, int rows_per_block,
+                                                    long long block_stride_w, long long block_stride_b,
+                                                    int n_rows_total, int dc, float* __restrict__ mod) {
+  __shared__ float s_c[kMaxCond];
+  for (int j = threadIdx.x; j < dc; j += blockDim.x) s_c[j] = cond_silu[j];
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  constexpr int kRowsPerWave = 4;
+  int row0 = (blockIdx.x * 4 + wave) * kRowsPerWave;
+  for (int rr = 0; rr < kRowsPerWave; ++rr) {
+    int row = row0 + rr;
+    if (row >= n_rows_total) return;
+    int blk = row / rows_per_block, r = row - blk * rows_per_block;
+    const T* wr = w + blk * block_stride_w + (long long)r * dc;
+    float acc = 0.f;
+    for (int j = lane; j < dc; j += 64) acc += to_f(wr[j]) * s_c[j];
+    acc = wave_sum(acc);
+    if (lane == 0) mod[row] = acc + b[blk * block_stride_b + r];
+  }
+}
+
+// h = LayerNorm(x) * (1 + scale) + shift per row (no affine, biased variance,
+// eps 1e-6), one wave per row, values held in registers between the passes.
+template <typename T, int MAXV>
+__global__ __launch_bounds__(256) void ln_mod_kernel(const float* __restrict__ x, const float* __restrict__ shift,
+                                                     const float* __restrict__ scale, T* __restrict__ out, int L,
+                                                     int C, const int* __restrict__ flag) {
+  if (flag != nullptr && *flag) return;
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= L) return;
+  const int C4 = C >> 2;
+  const float4* xr = reinterpret_cast<const float4*>(x + (long long)row * C);
+  float4 v[MAXV];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    int c4 = lane + i * 64;
+    if (c4 < C4) {
+      v[i] = xr[c4];
+      s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
+    }
+  }
+  const float mu = wave_sum(s) / (float)C;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    int c4 = lane + i * 64;
+    if (c4 < C4) {
+      float a = v[i].x - mu, bb = v[i].y - mu, c = v[i].z - mu, d = v[i].w - mu;
+      q += (a * a + bb * bb) + (c * c + d * d);
+    }
+  }
+  const float var = wave_sum(q) / (float)C;
+  const float rstd = 1.0f / sqrtf(var + 1e-6f);
+  T* orow = out + (long long)row * C;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    int c4 = lane + i * 64;
+    if (c4 < C4) {
+      float4 sc = reinterpret_cast<const float4*>(scale)[c4];
+      float4 sh = reinterpret_cast<const float4*>(shift)[c4];
+      int c = c4 * 4;
+      orow[c + 0] = to_t<T>((v[i].x - mu) * rstd * (1.f + sc.x) + sh.x);
+      orow[c + 1] = to_t<T>((v[i].y - mu) * rstd * (1.f + sc.y) + sh.y);
+      orow[c + 2] = to_t<T>((v[i].z - mu) * rstd * (1.f + sc.z) + sh.z);
+      orow[c + 3] = to_t<T>((v[i].w - mu) * rstd * (1.f + sc.w) + sh.w);
+    }
+  }
+}
+
+// QK RMSNorm and scatter.  Input: qkv [Mpad][3C] float (bias added).  One
+// workgroup per (64-token tile, head):
+//   q  -> rms(q) * gq       -> Q  [H][Mpad][D]
+//   k  -> rms(k) * gk       -> K  cache [H][Lcap][D] at row kv_off + m
+//   v                       -> V^T cache [H][D][Lcap] at column kv_off + m
+// The V tile is transposed through LDS so the V^T rows are written coalesced.
+template <typename T>
+__global__ __launch_bounds__(256) void qk_norm_kernel(const float* __restrict__ qkv, const float* __restrict__ gq,
+                                                      const float* __restrict__ gk, T* __restrict__ q,
+                                                      T* __restrict__ kring, T* __restrict__ vtring, int L, int H,
+                                                      int D, int Mpad, int Lcap, int kv_off,
+                                                      const int* __restrict__ flag) {
+  if (flag != nullptr && *flag) return;
+  __shared__ float s_v[64][129];
+  const int tile = blockIdx.x, h = blockIdx.y;
+  const int C = H * D;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int m0 = tile * 64;
+  // q and k: each wave takes 16 tokens
+  for (int i = 0; i < 16; ++i) {
+    int tl = wave * 16 + i;
+    int m = m0 + tl;
+    if (m >= L) break;
+    const float* row = qkv + (long long)m * 3 * C + h * D;
+#pragma unroll
+    for (int part = 0; part < 2; ++part) {
+      const float* src = row + part * C;
+      const float* g = part == 0 ? gq : gk;
+      float a0 = lane < D ? src[lane] : 0.f;
+      float a1 = lane + 64 < D ? src[lane + 64] : 0.f;
+      float ss = wave_sum(a0 * a0 + a1 * a1);
+      float r = 1.0f / sqrtf(ss / (float)D + 1e-6f);
+      T* dst = part == 0 ? q + ((long long)h * Mpad + m) * D : kring + ((long long)h * Lcap + kv_off + m) * D;
+      if (lane < D) dst[lane] = to_t<T>(a0 * r * g[lane]);
+      if (lane + 64 < D) dst[lane + 64] = to_t<T>(a1 * r * g[lane + 64]);
+    }
+    const float* vsrc = row + 2 * C;
+    if (lane < D) s_v[tl][lane] = vsrc[lane];
+    if (lane + 64 < D) s_v[tl][lane + 64] = vsrc[lane + 64];
+  }
+  __syncthreads();
+  // V^T: row dd holds 64 consecutive tokens
+  const int nt = min(64, L - m0);
+  for (int idx = threadIdx.x; idx < D * 64; idx += 256) {
+    int dd = idx >> 6, tl = idx & 63;
+    if (tl < nt) vtring[((long long)h * D + dd) * Lcap + kv_off + m0 + tl] = to_t<T>(s_v[tl][dd]);
+  }
+}
+
+// Skipped block (Eq. 4): out = x + rhat; runs only when the skip flag is set.
+template <typename T>
+__global__ __launch_bounds__(256) void skip_add_kernel(const float* __restrict__ x, const T* __restrict__ rhat,
+                                                       float* __restrict__ out, long long n4,
+                                                       const int* __restrict__ flag) {
+  if (*flag == 0) return;
+  for (long long i = blockIdx.x * 256ll + threadIdx.x; i < n4; i += (long long)gridDim.x * 256) {
+    float4 a = reinterpret_cast<const float4*>(x)[i];
+    const T* r = rhat + i * 4;
+    float4 o;
+    o.x = a.x + to_f(r[0]);
+    o.y = a.y + to_f(r[1]);
+    o.z = a.z + to_f(r[2]);
+    o.w = a.w + to_f(r[3]);
+    reinterpret_cast<float4*>(out)[i] = o;
+  }
+}
+
+__global__ void axpby_kernel(float a, const float* __restrict__ x, float b, const float* __restrict__ y,
+                             float* __restrict__ out, long long n) {
+  for (long long i = blockIdx.x * 256ll + threadIdx.x; i < n; i += (long long)gridDim.x * 256)
+    out[i] = a * x[i] + b * y[i];
+}
+
+__global__ void fill_f32_kernel(float* p, float v, long long n) {
+  for (long long i = blockIdx.x * 256ll + threadIdx.x; i < n; i += (long long)gridDim.x * 256) p[i] = v;
+}
+
+__global__ void pass_begin_kernel(GateState gs, int n_blocks) {
+  for (int b = threadIdx.x; b < n_blocks; b += blockDim.x) {
+    gs.rec_dec[b] = 2;  // forced unless a decision kernel evaluates the block
+    gs.rec_s[b] = __builtin_nanf("");
+    gs.rec_d[b] = __builtin_nanf("");
+    gs.rec_tau[b] = __builtin_nanf("");
+    gs.flags[b] = 0;
+  }
+}
+
+int grid_for(long long n, int per_block) {
+  long long g = (n + per_block - 1) / per_block;
+  if (g > 8192) g = 8192;
+  if (g < 1) g = 1;
+  return (int)g;
+}
+
+}  // namespace
+
+void launch_cond(const float* action, int temb_dim, int action_dim, float timestep, float* cond_silu,
+                 hipStream_t st) {
+  CondArgs a;
+  for (int i = 0; i < kMaxAction; ++i) a.action[i] = i < action_dim ? action[i] : 0.f;
+  cond_kernel<<<1, 256, 0, st>>>(a, temb_dim, action_dim, timestep, cond_silu);
+}
+
+void launch_adaln(int dtype, const void* w_ada, const float* b_ada, const float* cond_silu, int rows_per_block,
+                  long long block_stride_w, int n_blocks, int dc, float* mod, hipStream_t st) {
+  // W_ada is [n_blocks][rows_per_block][dc] and b_ada [n_blocks][rows_per_block]:
+  // block_stride_w = rows_per_block * dc, the bias stride is rows_per_block.
+  int total = rows_per_block * n_blocks;
+  int grid = (total + 15) / 16;
+  if (dtype == 1)
+    adaln_kernel<bf16><<<grid, 256, 0, st>>>((const bf16*)w_ada, b_ada, cond_silu, rows_per_block, block_stride_w,
+                                             rows_per_block, total, dc, mod);
+  else
+    adaln_kernel<float><<<grid, 256, 0, st>>>((const float*)w_ada, b_ada, cond_silu, rows_per_block,
+                                              block_stride_w, rows_per_block, total, dc, mod);
+}
+
+void launch_ln_mod(int dtype, const float* x, const float* shift, const float* scale, void* out, int L, int C,
+                   const int* flag, hipStream_t st) {
+  int grid = (L + 3) / 4;
+  int maxv = (C / 4 + 63) / 64;
+#define XC_LN(T, MV) ln_mod_kernel<T, MV><<<grid, 256, 0, st>>>(x, shift, scale, (T*)out, L, C, flag)
+  if (dtype == 1) {
+    if (maxv <= 2) XC_LN(bf16, 2);
+    else if (maxv <= 8) XC_LN(bf16, 8);
+    else XC_LN(bf16, 16);
+  } else {
+    if (maxv <= 2) XC_LN(float, 2);
+    else if (maxv <= 8) XC_LN(float, 8);
+    else XC_LN(float, 16);
+  }
+#undef XC_LN
+}
+
+void launch_qk_norm(int dtype, const float* qkv, const float* gq, const float* gk, void* q, void* kring,
+                    void* vtring, int L, int H, int D, int Mpad, int Lcap, int kv_off, const int* flag,
+                    hipStream_t st) {
+  dim3 grid((L + 63) / 64, H);
+  if (dtype == 1)
+    qk_norm_kernel<bf16><<<grid, 256, 0, st>>>(qkv, gq, gk, (bf16*)q, (bf16*)kring, (bf16*)vtring, L, H, D, Mpad,
+                                               Lcap, kv_off, flag);
+  else
+    qk_norm_kernel<float><<<grid, 256, 0, st>>>(qkv, gq, gk, (float*)q, (float*)kring, (float*)vtring, L, H, D,
+                                                Mpad, Lcap, kv_off, flag);
+}
+
+void launch_skip_add(int dtype, const float* x, const void* rhat, float* out, long long n, const int* flag,
+                     hipStream_t st) {
+  long long n4 = n / 4;
+  int grid = grid_for(n4, 256 * 4);
+  if (dtype == 1)
+    skip_add_kernel<bf16><<<grid, 256, 0, st>>>(x, (const bf16*)rhat, out, n4, flag);
+  else
+    skip_add_kernel<float><<<grid, 256, 0, st>>>(x, (const float*)rhat, out, n4, flag);
+}
+
+void launch_axpby(float a, const float* x, float b, const float* y, float* out, long long n, hipStream_t st) {
+  axpby_kernel<<<grid_for(n, 256 * 4), 256, 0, st>>>(a, x, b, y, out, n);
+}
+
+void launch_fill_f32(float* p, float v, long long n, hipStream_t st) {
+  fill_f32_kernel<<<grid_for(n, 256 * 4), 256, 0, st>>>(p, v, n);
+}
+
+void launch_pass_begin(const GateState& gs, int n_blocks, hipStream_t st) {
+  pass_begin_kernel<<<1, 256, 0, st>>>(gs, n_blocks);
+}
+
+}  // namespace xc

@@ -1,0 +1,109 @@
+// Internal declarations shared by the HIP kernels and the host orchestration.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace xc {
+
+typedef __bf16 bf16;
+
+// Maximum number of fingerprint view groups and conditioning values.
+constexpr int kMaxGroups = 8;
+constexpr int kMaxCond = 512;
+constexpr int kMaxAction = 64;
+
+// Rows per partial column-sum chunk of the fingerprint's global channel.
+constexpr int kFpChunkRows = 16;
+// Columns per workgroup of the fingerprint comparison kernel.
+constexpr int kFpCompareCols = 32;
+// Doubles per (workgroup, group) partial record of the comparison kernel.
+constexpr int kFpRecord = 8;
+
+// GEMM epilogue modes.
+enum EpiMode : int {
+  EPI_BIAS_F32 = 0,  // out_f32[m][n] = acc + bias[n]
+  EPI_OPROJ = 1,     // out_f32 = resid + gate * (acc + bias)          (x1)
+  EPI_UP = 2,        // out_t  = gelu_tanh(acc + bias)                   (u)
+  EPI_DOWN = 3,      // out_f32 = resid + gate * (acc + bias)  (y); out_t = y - xin (cached residual)
+};
+
+struct EpiArgs {
+  int M;               // valid rows
+  int N;               // columns (row stride of every output)
+  const float* bias;   // [N]
+  float* out_f32;      // see EpiMode
+  void* out_t;         // see EpiMode (element type = model dtype), may be null for EPI_DOWN
+  const float* resid;  // [M][N]
+  const float* gate;   // [N]
+  const float* xin;    // [M][N]
+};
+
+// Per-pass gate hyper-parameters handed to the decision kernel.
+struct GateArgs {
+  int adaptive;
+  float tau_floor, margin, alpha, tau_cos_fixed, tau_dev, eps;
+  int max_stale;
+  int strict0;          // 1 when this is step 0 in strict mode
+  float tau_strict0;
+  int n_groups;
+  int action_dim;       // 0: no action channel this pass
+  float action[kMaxAction];
+  float action_prev[kMaxAction];
+  int spatial_count[kMaxGroups];  // entries in each group's spatial fingerprint
+};
+
+// Gate state pointers (device).
+struct GateState {
+  float* ema;          // [S][B], NaN = unset
+  int* stale;          // [S][B]
+  int* skip_counts;    // [S][B]
+  int* flags;          // [B] skip flag of the current pass
+  int* rec_dec;        // [B] decision code of the last denoising pass
+  float* rec_s;        // [B]
+  float* rec_d;        // [B]
+  float* rec_tau;      // [B]
+};
+
+// Fingerprint tables (device).
+struct FpTables {
+  int n_chunks;              // partial column-sum chunks
+  const int4* chunks;        // {row_start, n_rows, camera, 0}
+  int n_cams;
+  const int* cam_chunk_begin;  // [n_cams + 1] prefix of chunks per camera
+  const int* cam_tokens;     // [n_cams]
+  int n_groups;
+  const int* grp_srow_begin; // [G + 1] spatial fingerprint rows per group (prefix)
+  const int* grp_cam_begin;  // [G + 1] cameras per group (prefix)
+  int n_srows;
+  const int* srows;          // [n_srows] global token row of each spatial row
+};
+
+// ---- launchers (each enqueues on `st`) -----------------------------------
+void launch_cond(const float* action, int temb_dim, int action_dim, float timestep, float* cond_silu,
+                 hipStream_t st);
+void launch_adaln(int dtype, const void* w_ada, const float* b_ada, const float* cond_silu, int rows_per_block,
+                  long long block_stride_w, int n_blocks, int dc, float* mod, hipStream_t st);
+void launch_ln_mod(int dtype, const float* x, const float* shift, const float* scale, void* out, int L, int C,
+                   const int* flag, hipStream_t st);
+void launch_gemm(int dtype, EpiMode mode, const void* A, const void* W, int M, int N, int K, const EpiArgs& e,
+                 const int* flag, hipStream_t st);
+void launch_qk_norm(int dtype, const float* qkv, const float* gq, const float* gk, void* q, void* kring,
+                    void* vtring, int L, int H, int D, int Mpad, int Lcap, int kv_off, const int* flag,
+                    hipStream_t st);
+void launch_attention(int dtype, const void* q, const void* kring, const void* vtring, void* o, int L, int Mpad,
+                      int Lcap, int Lk, int H, int D, const int* flag, hipStream_t st);
+void launch_skip_add(int dtype, const float* x, const void* rhat, float* out, long long n, const int* flag,
+                     hipStream_t st);
+void launch_axpby(float a, const float* x, float b, const float* y, float* out, long long n, hipStream_t st);
+void launch_pass_begin(const GateState& gs, int n_blocks, hipStream_t st);
+void launch_fp_colsum(const float* x, int C, const FpTables& t, float* partial, hipStream_t st);
+void launch_fp_compare(const float* x, int C, const FpTables& t, const float* partial, float* fp_prev,
+                       double* records, hipStream_t st);
+int fp_compare_groups_of_wg(int C);
+void launch_gate_decide(const double* records, int n_wg, const GateArgs& ga, const GateState& gs, int S_idx,
+                        int b, int n_blocks, int evaluate, hipStream_t st);
+void launch_fill_f32(float* p, float v, long long n, hipStream_t st);
+
+}  // namespace xc

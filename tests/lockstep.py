@@ -1,0 +1,134 @@
+"""Lock-step rollout of the HIP library and the CPU oracle on the same seeded
+stream, comparing every pass.
+
+Decisions: where the oracle evaluates the gate, the device's decision must be
+the oracle's, except when one of the oracle's metrics lies within a relative
+1e-3 of its threshold -- there either decision is correct, and the oracle then
+follows the device's branch so the two stay comparable afterwards.  The
+oracle's own metrics, EMA and fingerprints are never taken from the device.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+import synth
+from oracle import xcache_oracle as xo
+
+BAND = 1e-3
+
+
+def rel_l2(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-30))
+
+
+def in_band(info, tau_dev):
+    s, tau, d = info["s"], info["tau"], info["d"]
+    near_s = abs(s - tau) <= BAND * max(abs(tau), 1e-12)
+    near_d = math.isfinite(tau_dev) and abs(d - tau_dev) <= BAND * max(abs(tau_dev), 1e-12)
+    return near_s or near_d
+
+
+class Lockstep:
+    def __init__(self, w: synth.Workload, weights=None, compute=np.float64, seed=0):
+        import torch
+        from paper_2604_20289_amd.xcache import XCache
+
+        self.torch = torch
+        self.w = w
+        self.m = w.model
+        self.blob = synth.make_weights(self.m, seed) if weights is None else weights
+        self.stream = torch.cuda.current_stream().cuda_stream
+        self.xc = XCache(self.m, w.gate, self.blob, self.stream)
+        self.orc = xo.XCacheOracle(self.m, w.gate, self.blob, compute)
+        self.seed = seed
+        self.band_hits = 0
+        self.decisions_checked = 0
+        self.worst = {}
+
+    def close(self):
+        self.xc.close()
+
+    def _decide(self, gpu_dec, log):
+        tau_dev = self.w.gate.tau_dev
+
+        def decide(b, info):
+            own = bool(info["skip"])
+            dev = int(gpu_dec[b])
+            assert dev in (xo.DEC_COMPUTE, xo.DEC_SKIP), f"block {b}: device did not evaluate (code {dev})"
+            dev_skip = dev == xo.DEC_SKIP
+            self.decisions_checked += 1
+            if dev_skip == own:
+                return own
+            if in_band(info, tau_dev):
+                self.band_hits += 1
+                return dev_skip
+            raise AssertionError(f"{log}: block {b} decision differs outside the band: oracle "
+                                 f"skip={own} s={info['s']:.9f} tau={info['tau']:.9f} d={info['d']:.6f}; "
+                                 f"device skip={dev_skip}")
+
+        return decide
+
+    def _compare(self, tag, got, want, tol_abs=None, tol_rel_l2=None):
+        if tol_abs is not None:
+            err = float(np.max(np.abs(got.astype(np.float64) - want)))
+            self.worst[tag] = max(self.worst.get(tag, 0.0), err)
+            assert err <= tol_abs, f"{tag}: max-abs {err:.3e} > {tol_abs:.1e}"
+        if tol_rel_l2 is not None:
+            err = rel_l2(got, want)
+            self.worst[tag] = max(self.worst.get(tag, 0.0), err)
+            assert err <= tol_rel_l2, f"{tag}: rel-L2 {err:.3e} > {tol_rel_l2:.1e}"
+
+    def run(self, n_chunks, tol_abs=None, tol_rel_l2=None, flags=lambda n, t: 0, on_pass=None):
+        torch = self.torch
+        m, w = self.m, self.w
+        L, C = m.tokens, m.hidden
+        taus = synth.timesteps(m)
+        eps_list = synth.latent_stream(m, w.stream, self.seed, n_chunks)
+        act_list = synth.action_stream(m, w.stream, self.seed, n_chunks)
+        dev = torch.device("cuda")
+        x_d = torch.empty((L, C), dtype=torch.float32, device=dev)
+        y_d = torch.empty_like(x_d)
+        k_d = torch.empty_like(x_d)
+        for n, eps, a in zip(range(n_chunks), eps_list, act_list):
+            eps_d = torch.from_numpy(eps).to(dev)
+            x_d.copy_(eps_d)
+            x_o = eps.astype(np.float64)
+            eps_o = eps.astype(np.float64)
+            for t in range(m.n_steps):
+                f = flags(n, t)
+                self.xc.forward_chunk(t, taus[t], a, x_d, y_d, f)
+                st = self.xc.stats()
+                tag = f"n={n} t={t}"
+                y_o = self.orc.forward_chunk(t, taus[t], a, x_o, f, self._decide(st["last_decision"], tag))
+                # where both evaluated, the reported metrics must agree closely
+                for b, info in enumerate(self.orc.last):
+                    if info["decision"] == xo.DEC_FORCED:
+                        assert st["last_decision"][b] == xo.DEC_FORCED, f"{tag} block {b}: device evaluated"
+                    else:
+                        assert abs(st["last_cos"][b] - info["s"]) <= 1e-4 + 1e-3 * (1 - min(info["s"], 1.0)), \
+                            (tag, b, st["last_cos"][b], info["s"])
+                        assert abs(st["last_tau"][b] - info["tau"]) <= 1e-4, (tag, b, st["last_tau"][b], info["tau"])
+                        if math.isfinite(info["d"]):
+                            assert abs(st["last_dev"][b] - info["d"]) <= 1e-3 * max(1.0, abs(info["d"])), \
+                                (tag, b, st["last_dev"][b], info["d"])
+                self._compare(tag, y_d.cpu().numpy(), y_o, tol_abs, tol_rel_l2)
+                if on_pass:
+                    on_pass(n, t, y_d, y_o, st)
+                if t + 1 < m.n_steps:
+                    sg = synth.sampler_sigma(m, t + 1)
+                    self.xc.axpby(1.0 - sg, y_d, sg, eps_d, x_d, L * C)
+                    x_o = (1.0 - sg) * y_o + sg * eps_o
+            self.xc.kv_update(synth.KV_UPDATE_TIMESTEP, a, y_d, k_d)
+            k_o = self.orc.kv_update(synth.KV_UPDATE_TIMESTEP, a, y_o)
+            torch.cuda.synchronize()
+            self._compare(f"n={n} kv", k_d.cpu().numpy(), k_o, tol_abs, tol_rel_l2)
+        st = self.xc.stats()
+        ost = self.orc.stats()
+        for key in ("generations", "evals_post_warmup", "gated_evals", "skips", "kv_block_evals"):
+            assert st[key] == ost[key], (key, st[key], ost[key])
+        np.testing.assert_array_equal(st["skip_counts"], ost["skip_counts"])
+        return st
