@@ -1,0 +1,264 @@
+"""Benchmark of the cached chunk forward on one MI355X.
+
+A step is one generation chunk: S denoising passes (with the sampler update
+between them) plus the KV-update pass, over the multi-camera bf16 DiT
+workload (20 blocks, hidden 1536, 12 heads x 128, MLP 6144; 6 cameras x 3
+latent frames x 15 x 26 patches = 7020 tokens; a 3-chunk key/value window =
+21060 keys; 4 steps).  Inputs are synthetic and seeded (weights N(0, 0.02^2),
+an AR(1) latent stream with rho 0.97, a 16-d action random walk with sigma
+0.03) and resident in HBM before the timed region; the gate uses Table 1's
+defaults.
+
+Runs, in order:
+  1. gate on, `warmup` untimed chunks then `steps` timed chunks -> chunk
+     latency (the reported value) and block skip rate;
+  2. gate off (every block computed, same kernels), same chunks, with HIP
+     events around every kernel launch -> full-compute latency, effective
+     block TFLOP/s, per-kernel durations and the roofline of the dominant
+     kernel (attention);
+  3. gate on again for two chunks with kernel events -> gate-kernel GB/s;
+  4. the CPU oracle on a bounded sample (one computed block at the full
+     shape, float64 numpy on the host cores), scaled to ms per chunk.
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+
+METRIC = "chunk latency ms + block TFLOP/s vs MFMA peak + block skip rate, 1 GPU"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def block_flops(m, n_keys):
+    L, C, Dm = m.tokens, m.hidden, m.mlp_hidden
+    return 6.0 * L * C * C + 2.0 * L * C * C + 4.0 * L * C * Dm + 4.0 * L * n_keys * C
+
+
+def attention_flops(m, n_keys):
+    return 4.0 * m.tokens * n_keys * m.n_heads * m.head_dim
+
+
+def run_stream(xc, m, eps_dev, actions, n_warm, n_timed, torch, profile=False, on_profile_start=None):
+    """Drive n_warm + n_timed chunks; returns per-chunk ms of the timed ones."""
+    L, C = m.tokens, m.hidden
+    taus = synth.timesteps(m)
+    x = torch.empty((L, C), dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    ms = []
+    for n in range(n_warm + n_timed):
+        eps = eps_dev[n]
+        timed = n >= n_warm
+        if timed and n == n_warm:
+            torch.cuda.synchronize()
+            if profile:
+                xc.profile(True)
+        if timed:
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+        x.copy_(eps)
+        for t in range(m.n_steps):
+            xc.forward_chunk(t, taus[t], actions[n], x, y)
+            if t + 1 < m.n_steps:
+                sg = synth.sampler_sigma(m, t + 1)
+                xc.axpby(1.0 - sg, y, sg, eps, x, L * C)
+        xc.kv_update(synth.KV_UPDATE_TIMESTEP, actions[n], y, None)
+        if timed:
+            e1.record()
+            ms.append((e0, e1))
+    torch.cuda.synchronize()
+    if profile:
+        xc.profile(False)
+    return [a.elapsed_time(b) for a, b in ms]
+
+
+def kernel_table(xc, xcp):
+    out = {}
+    for k in range(xcp.XC_KERN_COUNT):
+        n, tot = xc.kernel_times(k, clear=True)
+        if n:
+            out[xcp.KERNEL_NAMES[k]] = {"launches": n, "avg_us": 1e3 * tot / n, "total_ms": tot}
+    return out
+
+
+def cpu_baseline(w, weights, seed):
+    """The oracle, as it is, on one computed block at the full shape (full key window)."""
+    from oracle import xcache_oracle as xo
+    m = w.model
+    small = synth.with_model(w, n_blocks=1).model
+    blob = weights[: synth.block_numel(m)]
+    orc = xo.XCacheOracle(small, synth.GateParams(enabled=0), blob)
+    rng = np.random.default_rng(seed + 7)
+    L, H, d = m.tokens, m.n_heads, m.head_dim
+    orc.ring[0] = [(xo.bf16_round(rng.standard_normal((H, L, d))), xo.bf16_round(rng.standard_normal((H, L, d))))
+                   for _ in range(m.kv_window - 1)]
+    x = next(synth.latent_stream(m, w.stream, seed, 1)).astype(np.float64)
+    cond = orc.cond(1000.0, np.zeros(m.action_dim))
+    t0 = time.perf_counter()
+    orc.block(0, x, cond)
+    dt = time.perf_counter() - t0
+    cores = len(os.sched_getaffinity(0))
+    per_chunk_ms = dt * 1e3 * m.n_blocks * (m.n_steps + 1)
+    return {"value": per_chunk_ms, "unit": "ms/chunk", "cores": cores, "kind": "oracle",
+            "sample": (f"one computed block at the full shape (L={L}, {m.kv_window * L} keys), float64 numpy, "
+                       f"{dt:.1f} s, scaled x{m.n_blocks * (m.n_steps + 1)} block evaluations to a full-compute "
+                       f"chunk")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=12, help="timed chunks")
+    ap.add_argument("--warmup", type=int, default=2, help="untimed chunks before them")
+    ap.add_argument("--workload", type=int, default=2, help="index of the synthetic workload preset")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--tau-floor", type=float, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-gate-off", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the cached chunk forward of one rollout runs on a single device "
+              "(several GPUs would each run their own rollout); run it with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2604_20289_amd import xcache as xcp
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    w = synth.workload(args.workload)
+    if args.tau_floor is not None:
+        w = synth.with_gate(w, tau_floor=args.tau_floor)
+    m = w.model
+    n_chunks = args.warmup + args.steps
+    log(f"workload {w.name}: L={m.tokens} blocks={m.n_blocks} chunks={n_chunks}")
+    t0 = time.time()
+    weights = synth.make_weights(m, args.seed)
+    eps_host = list(synth.latent_stream(m, w.stream, args.seed, n_chunks))
+    actions = list(synth.action_stream(m, w.stream, args.seed, n_chunks))
+    eps_dev = [torch.from_numpy(e).cuda() for e in eps_host]
+    del eps_host
+    log(f"inputs ready in {time.time() - t0:.1f} s")
+    stream = torch.cuda.current_stream().cuda_stream
+
+    # 1. gate on
+    xc = xcp.XCache(m, w.gate, weights, stream)
+    on_ms = run_stream(xc, m, eps_dev, actions, args.warmup, args.steps, torch)
+    st = xc.stats()
+    # 3. gate kernels (same handle, two more chunks continue the stream state)
+    xc.reset()
+    prof_chunks = min(n_chunks, 3)
+    run_stream(xc, m, eps_dev, actions, prof_chunks - 1, 1, torch, profile=True)
+    gate_k = kernel_table(xc, xcp)
+    xc.close()
+    log(f"gate on: median {statistics.median(on_ms):.2f} ms/chunk, skips {st['skips']} / "
+        f"{st['evals_post_warmup']}")
+
+    # 2. gate off
+    off_ms, kt = None, {}
+    if not args.no_gate_off:
+        xc = xcp.XCache(m, synth.with_gate(w, enabled=0).gate, weights, stream)
+        off_ms = run_stream(xc, m, eps_dev, actions, args.warmup, args.steps, torch, profile=True)
+        kt = kernel_table(xc, xcp)
+        xc.close()
+        log(f"gate off: median {statistics.median(off_ms):.2f} ms/chunk")
+
+    Lk = m.kv_window * m.tokens  # every timed chunk sees the full window (warmup >= window - 1)
+    steady = args.warmup >= m.kv_window - 1
+    fl_block = block_flops(m, Lk)
+    B, S = m.n_blocks, m.n_steps
+    # skip rate over the timed chunks' denoising block evaluations (warmup chunks excluded)
+    skip_rate = st["skips"] / max(1, st["evals_post_warmup"])
+    on_med = statistics.median(on_ms)
+    res = {
+        "metric": METRIC,
+        "value": round(on_med, 3),
+        "unit": "ms/chunk",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(statistics.mean(on_ms), 3),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "blocks": B, "hidden": m.hidden, "heads": m.n_heads,
+                   "head_dim": m.head_dim, "mlp_hidden": m.mlp_hidden, "tokens_per_chunk": m.tokens,
+                   "kv_window_chunks": m.kv_window, "keys": Lk, "denoising_steps": S,
+                   "stream_rho": w.stream.rho, "gate": "Table 1 defaults" if args.tau_floor is None
+                   else f"Table 1 with tau_floor={args.tau_floor}", "steady_state_window": steady},
+        "skip_rate": round(skip_rate, 4),
+        "skips": st["skips"],
+        "block_evals_post_warmup": st["evals_post_warmup"],
+    }
+    if off_ms:
+        off_med = statistics.median(off_ms)
+        chunk_flops = fl_block * B * (S + 1)
+        res["full_compute_ms"] = round(off_med, 3)
+        res["speedup_vs_full_compute"] = round(off_med / on_med, 3)
+        res["block_tflops_effective"] = round(chunk_flops / (off_med * 1e-3) / 1e12, 1)
+        res["block_mfma_frac_effective"] = round(res["block_tflops_effective"] / PEAK_BF16_TFLOPS, 4)
+        contraction_ms = sum(kt[k]["total_ms"] for k in ("attention", "gemm_qkv", "gemm_oproj", "gemm_up",
+                                                         "gemm_down") if k in kt)
+        n_blocks_timed = args.steps * B * (S + 1)
+        if contraction_ms > 0:
+            res["block_tflops_kernels"] = round(fl_block * n_blocks_timed / (contraction_ms * 1e-3) / 1e12, 1)
+        if "attention" in kt:
+            a = kt["attention"]
+            af = attention_flops(m, Lk)
+            ach = af / (a["avg_us"] * 1e-6) / 1e12
+            res["roofline"] = {"kernel": "attention", "bound": "mfma", "achieved": round(ach, 1),
+                               "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
+                               "traffic": None, "flops_per_launch": af, "avg_launch_us": round(a["avg_us"], 1)}
+        gem = {"gemm_qkv": 6.0, "gemm_oproj": 2.0, "gemm_up": 2.0 * m.mlp_hidden / m.hidden,
+               "gemm_down": 2.0 * m.mlp_hidden / m.hidden}
+        res["kernels_full_compute"] = {}
+        for k, v in kt.items():
+            e = {"launches": v["launches"], "avg_us": round(v["avg_us"], 2)}
+            if k in gem:
+                f = gem[k] * m.tokens * m.hidden * m.hidden
+                e["tflops"] = round(f / (v["avg_us"] * 1e-6) / 1e12, 1)
+            if k == "attention":
+                e["tflops"] = res["roofline"]["achieved"]
+            if k == "ln_mod":
+                e["gbs"] = round(6.0 * m.tokens * m.hidden / (v["avg_us"] * 1e-6) / 1e9, 1)
+            res["kernels_full_compute"][k] = e
+    gk = {}
+    L, C = m.tokens, m.hidden
+    for k, v in gate_k.items():
+        e = {"launches": v["launches"], "avg_us": round(v["avg_us"], 2)}
+        if k == "gate_reduce":
+            e["gbs"] = round(4.0 * L * C / (v["avg_us"] * 1e-6) / 1e9, 1)
+            e["hbm_frac"] = round(e["gbs"] / PEAK_HBM_GBS, 4)
+        if k == "skip_add":
+            e["note"] = "averaged over launches that add and launches that return at entry"
+        gk[k] = e
+    res["kernels_gate_on"] = gk
+    if not args.no_cpu_baseline:
+        log("cpu baseline: one oracle block at full shape ...")
+        res["cpu_baseline"] = cpu_baseline(w, weights, args.seed)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()
