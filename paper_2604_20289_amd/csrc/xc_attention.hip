@@ -43,22 +43,42 @@ __device__ __forceinline__ int row_of_key(int key) {
   return mt * 32 + g * 8 + hh * 4 + r;
 }
 
-// Workgroups are dispatched round-robin over the 8 XCDs (each with its own
-// L2).  The 1-D grid is remapped so that XCD x runs a contiguous range of
-// (head, query-tile) items: the query tiles of one head then stream the same
-// key/value tiles through one L2 at about the same time.
 constexpr int kXcds = 8;
 
+__device__ __forceinline__ float partner_max(float x) {
+  // max(x, x of lane ^ 32): v_permlane32_swap exchanges the two half-waves
+  // (a VALU operation, no LDS round trip)
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float partner_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Work distribution.  An item is (head, 128-query tile); its key tiles are
+// split into S equal chunks, S chosen by the launcher so that the units
+// (item, chunk) fill whole rounds of resident workgroups (two per CU).  Units
+// are ordered [head][chunk][query tile] and dealt to the 8 XCDs (each with
+// its own L2) in contiguous ranges (workgroups are dispatched round-robin
+// over the XCDs, so workgroup b takes unit (b mod 8) * per_xcd + b / 8): the
+// workgroups resident on one XCD then stream the same key/value chunk of one
+// head at about the same time.  With S = 1 a unit writes the normalised
+// output; otherwise it leaves (O unnormalised, running max, running sum) in
+// the workspace and the merge kernel combines the S pieces of each item.
+//
+// Software pipeline, per wave and key tile j:
+//   S(j+1) = K(j+1) Q^T on the MFMA pipe, while the VALU runs the softmax of
+//   S(j); then O^T += V(j)^T P(j)^T.  K runs one tile ahead of V in LDS:
+//   iteration j reads K(j+1) and V(j) and refills K(j+2) and V(j+1).
 template <int D>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ Kc,
                                                            const bf16* __restrict__ Vt, bf16* __restrict__ O, int L,
-                                                           int Mpad, int Lcap, int Lk, int H, int n_qt, float sl2,
+                                                           int Mpad, int Lcap, int Lk, int H, int n_qt, int n_split,
+                                                           float sl2, float* __restrict__ ws,
                                                            const int* __restrict__ flag) {
   if (flag != nullptr && *flag) return;
-  const int total = H * n_qt;
-  const int per_xcd = (total + kXcds - 1) / kXcds;
-  const int item = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
-  if (item >= total) return;
   constexpr int KCH = D / 8;                // 16-byte chunks per key row
   constexpr int KLD = 64 * KCH / 256;       // K chunks staged per thread
   constexpr int VLD = D * 8 / 256;          // V^T chunks staged per thread
@@ -72,76 +92,90 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* __restric
   __shared__ __attribute__((aligned(16))) bf16 sV[2][D * VR];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hi = lane >> 5, lo = lane & 31;
-  const int h = item / n_qt;
-  const int q0 = (item - h * n_qt) * 128 + wave * 32;
   const int C = H * D;
+  const int NT = (Lk + 63) / 64;
+  const int units = H * n_split * n_qt;
+  const int per_xcd = (units + kXcds - 1) / kXcds;
+  const int unit = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+  if (unit >= units) return;
+  const int h = unit / (n_split * n_qt);
+  const int rem = unit - h * n_split * n_qt;
+  const int kc = rem / n_qt, qt = rem - kc * n_qt;
+  const int k0 = (int)((long long)kc * NT / n_split), k1 = (int)((long long)(kc + 1) * NT / n_split);
+  const int q0 = qt * 128 + wave * 32;
 
-  bf16x8 qf[D / 16];
-  {
-    const bf16* qrow = Q + ((long long)h * Mpad + q0 + lo) * D + hi * 8;
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) qf[ks] = *reinterpret_cast<const bf16x8*>(qrow + ks * 16);
-  }
-  // per-thread staging sources (advanced by one tile per step) and LDS slots
-  const bf16* kg[KLD];
-  const bf16* vg[VLD];
-  int ks_off[KLD], vs_off[VLD];
-#pragma unroll
-  for (int i = 0; i < KLD; ++i) {
-    const int q = tid + 256 * i, key = q / KCH, c = q % KCH;
-    kg[i] = Kc + ((long long)h * Lcap + key) * D + c * 8;
-    ks_off[i] = row_of_key(key) * KR + c * 8;
-  }
-#pragma unroll
-  for (int i = 0; i < VLD; ++i) {
-    const int q = tid + 256 * i, dd = q >> 3, c = q & 7;
-    vg[i] = Vt + ((long long)h * D + dd) * Lcap + c * 8;
-    vs_off[i] = dd * VR + c * 8;
-  }
+  // thread tid stages K rows key0 + (256/KCH) i and V^T rows dd0 + 32 i: one
+  // per-thread offset each, the i-steps are wave-uniform (row_of_key maps
+  // key + 16 i to its row + 16 i for key < 16)
+  static_assert(256 / KCH == 16 || 256 / KCH == 32, "staging layout");
+  constexpr int KSTEP = 256 / KCH;
+  const int key0 = tid / KCH, kc0 = tid % KCH;
+  const int kg0 = (key0 * D + kc0 * 8) * 2;
+  const int ks0 = row_of_key(key0) * KR + kc0 * 8;
+  const int dd0 = tid >> 3, vc0 = tid & 7;
+  const int vg0 = (dd0 * Lcap + vc0 * 8) * 2;
+  const int vs0 = dd0 * VR + vc0 * 8;
   const int k_frag = lo * KR + hi * 8;   // + mt*32*KR + ks*16
   const int v_frag = lo * VR + hi * 8;   // + dt*32*VR + kv*16
-
-  f32x16 oacc[DT];
-#pragma unroll
-  for (int i = 0; i < DT; ++i)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) oacc[i][r] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
   const float lazy = 8.0f / sl2;
 
-  u32x4 rk[KLD], rv[VLD];
-  auto gload = [&](int j) __attribute__((always_inline)) {
+  {
+    bf16x8 qf[D / 16];
+    {
+      const bf16* qrow = Q + ((long long)h * Mpad + q0 + lo) * D + hi * 8;
 #pragma unroll
-    for (int i = 0; i < KLD; ++i) rk[i] = *reinterpret_cast<const u32x4*>(kg[i] + (long long)j * 64 * D);
-#pragma unroll
-    for (int i = 0; i < VLD; ++i) rv[i] = *reinterpret_cast<const u32x4*>(vg[i] + j * 64);
-  };
-  auto sstore = [&](int buf) __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < KLD; ++i) *reinterpret_cast<u32x4*>(&sK[buf][ks_off[i]]) = rk[i];
-#pragma unroll
-    for (int i = 0; i < VLD; ++i) *reinterpret_cast<u32x4*>(&sV[buf][vs_off[i]]) = rv[i];
-  };
-
-  const int NT = (Lk + 63) / 64;
-  auto step = [&](int j, int cur) __attribute__((always_inline)) {
-    if (j + 1 < NT) gload(j + 1);
-    f32x16 sacc[2];
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[mt][r] = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < D / 16; ++ks) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&sK[cur][k_frag + mt * 32 * KR + ks * 16]);
-        sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], sacc[mt], 0, 0, 0);
-      }
+      for (int ks = 0; ks < D / 16; ++ks) qf[ks] = *reinterpret_cast<const bf16x8*>(qrow + ks * 16);
     }
-    // running max in raw score units; p = 2^(s*c - m*c) with c = log2(e)/sqrt(d).
-    // The rescale of the output accumulators is skipped while the max has
-    // grown by less than 8/c since the last rescale (p then stays <= 2^8,
-    // harmless for the float sums and the bf16 probabilities).
-    if ((j + 1) * 64 > Lk) {  // last tile: mask keys past the window
+    // staging sources: a wave-uniform per-head base plus 32-bit per-thread
+    // byte offsets (the tile advance is a scalar add on the base)
+    const char* Kh = reinterpret_cast<const char*>(Kc + (long long)h * Lcap * D);
+    const char* Vh = reinterpret_cast<const char*>(Vt + (long long)h * D * Lcap);
+
+    f32x16 oacc[DT];
+#pragma unroll
+    for (int i = 0; i < DT; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[i][r] = 0.f;
+    float m_run = -INFINITY, l_run = 0.f;
+
+    u32x4 rk[KLD], rv[VLD];
+    auto load_k = [&](int j) __attribute__((always_inline)) {
+#pragma unroll
+      for (int i = 0; i < KLD; ++i) {
+        const char* base = Kh + ((long long)j * 64 + i * KSTEP) * D * 2;
+        rk[i] = *reinterpret_cast<const u32x4*>(base + kg0);
+      }
+    };
+    auto load_v = [&](int j) __attribute__((always_inline)) {
+#pragma unroll
+      for (int i = 0; i < VLD; ++i) {
+        const char* base = Vh + ((long long)i * 32 * Lcap + j * 64) * 2;
+        rv[i] = *reinterpret_cast<const u32x4*>(base + vg0);
+      }
+    };
+    auto store_k = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+      for (int i = 0; i < KLD; ++i) *reinterpret_cast<u32x4*>(&sK[buf][ks0 + i * KSTEP * KR]) = rk[i];
+    };
+    auto store_v = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+      for (int i = 0; i < VLD; ++i) *reinterpret_cast<u32x4*>(&sV[buf][vs0 + i * 32 * VR]) = rv[i];
+    };
+    auto qk = [&](f32x16* sacc, int buf) __attribute__((always_inline)) {
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sacc[mt][r] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < D / 16; ++ks)
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt) {
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(&sK[buf][k_frag + mt * 32 * KR + ks * 16]);
+          sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], sacc[mt], 0, 0, 0);
+        }
+    };
+    // keys past the window (last tile only) get -inf scores
+    auto mask = [&](f32x16* sacc, int j) __attribute__((always_inline)) {
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
@@ -149,74 +183,219 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* __restric
           const int key = j * 64 + key_of_row(mt, (i >> 2) * 8 + hi * 4 + (i & 3));
           if (key >= Lk) sacc[mt][i] = -INFINITY;
         }
+    };
+    auto tile_max = [&](const f32x16* sacc) __attribute__((always_inline)) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[mt][i]);
+      return partner_max(mx);
+    };
+    // probabilities of one score tile against the settled running max m_run
+    // (raw score units): p = 2^(s c - m c), c = log2(e)/sqrt(d)
+    auto probs = [&](f32x16* sacc, bf16x8* pb) __attribute__((always_inline)) {
+      const float msc = -m_run * sl2;
+      float ps = 0.f;
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(sacc[mt][i], sl2, msc));
+          sacc[mt][i] = p;
+          ps += p;
+        }
+      l_run += ps;
+#pragma unroll
+      for (int kv = 0; kv < 4; ++kv)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) pb[kv][i] = (bf16)sacc[kv >> 1][(kv & 1) * 8 + i];
+    };
+    auto pv = [&](const bf16x8* pb, int buf) __attribute__((always_inline)) {
+#pragma unroll
+      for (int kv = 0; kv < 4; ++kv)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(&sV[buf][v_frag + dt * 32 * VR + kv * 16]);
+          oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kv], oacc[dt], 0, 0, 0);
+        }
+    };
+    // The running max moves only when a tile's max exceeds it by more than
+    // 8/c (p then stays <= 2^8 in between, harmless for the float sums and
+    // the bf16 probabilities); the rescale then also covers the tile just
+    // added.
+    auto update_max = [&](float mx) __attribute__((always_inline)) {
+      if (mx > m_run + lazy) {
+        const float alpha = __builtin_amdgcn_exp2f((m_run - mx) * sl2);
+        l_run *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
+        m_run = mx;
+      }
+    };
+
+    // prologue: K(k0), V(k0), K(k0+1) in LDS; S(k0) and its max
+    load_k(k0);
+    load_v(k0);
+    store_k(0);
+    store_v(0);
+    if (k0 + 1 < k1) {
+      load_k(k0 + 1);
+      store_k(1);
     }
-    float mx = -INFINITY;
+    __syncthreads();
+    f32x16 sa[2], sb[2];
+    qk(sa, 0);
+    if (k0 == NT - 1) mask(sa, k0);
+    m_run = tile_max(sa);
+    __syncthreads();  // the first iteration refills K buffer 0, which S(k0) just read
+
+    // Iteration j (local index jj = j - k0; scur = S(j), its max already in m_run):
+    //   region 1: S(j+1) MFMAs from K buffer kb_next  ||  probabilities of S(j)
+    //   region 2: PV(j) MFMAs from V buffer vb_cur     ||  max of S(j+1)
+    //   then the (rare) rescale and the refills K(j+2) -> vb_cur, V(j+1) -> kb_next.
+    // The steady-state loop calls it with constant buffer arguments and no
+    // mask: no branch inside.
+    auto iter = [&](int j, f32x16* scur, f32x16* snext, int kb_next, int vb_cur, bool has_next, bool mask_next)
+        __attribute__((always_inline)) {
+      const bool more_k = j + 2 < k1;
+      if (more_k) load_k(j + 2);
+      if (has_next) load_v(j + 1);
+      if (has_next) qk(snext, kb_next);
+      bf16x8 pb[4];
+      probs(scur, pb);
+      pv(pb, vb_cur);
+      if (has_next) {
+        if (mask_next) mask(snext, j + 1);
+        update_max(tile_max(snext));
+      }
+      if (more_k) store_k(vb_cur);
+      if (has_next) store_v(kb_next);
+      __syncthreads();
+    };
+    const int n = k1 - k0;
+    const int n_reg = n > 2 ? n - 2 : 0;  // iterations whose next tile is not the segment's last
+    int jj = 0;
+    for (; jj + 1 < n_reg; jj += 2) {
+      iter(k0 + jj, sa, sb, 1, 0, true, false);
+      iter(k0 + jj + 1, sb, sa, 0, 1, true, false);
+    }
+    if (jj < n_reg) {
+      iter(k0 + jj, sa, sb, 1, 0, true, false);
+      ++jj;
+    }
+    // the last two iterations: the next tile may be the masked global last
+    // one, then there is no next tile
+    const bool mask_last = (Lk & 63) != 0 && k1 == NT;
+    if ((jj & 1) == 0) {
+      if (jj + 1 < n) {
+        iter(k0 + jj, sa, sb, 1, 0, true, mask_last);
+        iter(k0 + jj + 1, sb, sa, 0, 1, false, false);
+      } else {
+        iter(k0 + jj, sa, sb, 1, 0, false, false);
+      }
+    } else {
+      if (jj + 1 < n) {
+        iter(k0 + jj, sb, sa, 0, 1, true, mask_last);
+        iter(k0 + jj + 1, sa, sb, 1, 0, false, false);
+      } else {
+        iter(k0 + jj, sb, sa, 0, 1, false, false);
+      }
+    }
+
+    const float l_tot = partner_sum(l_run);
+    const int q = q0 + lo;
+    if (n_split == 1) {
+      // whole item in this unit: normalised output
+      const float inv = 1.0f / l_tot;
+      if (q < L) {
+        bf16* orow = O + (long long)q * C + h * D;
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
+        for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[mt][i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    if (mx > m_run + lazy) {
-      const float m_new = fmaxf(mx, m_run);
-      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * sl2);
-      l_run *= alpha;
+          for (int g = 0; g < 4; ++g) {
+            const int dd = dt * 32 + g * 8 + hi * 4;
+            typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+            bf16x4 o4;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) o4[r] = (bf16)(oacc[dt][g * 4 + r] * inv);
+            *reinterpret_cast<bf16x4*>(orow + dd) = o4;
+          }
+      }
+    } else {
+      // partial: O (unnormalised) [128][D], then running max and sum [128] each
+      const int item = h * n_qt + qt;
+      float* wo = ws + ((long long)item * n_split + kc) * (128 * D + 256);
+      const int ql = wave * 32 + lo;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
-      m_run = m_new;
+        for (int g = 0; g < 4; ++g) {
+          const int dd = dt * 32 + g * 8 + hi * 4;
+          float4 o4 = {oacc[dt][g * 4], oacc[dt][g * 4 + 1], oacc[dt][g * 4 + 2], oacc[dt][g * 4 + 3]};
+          *reinterpret_cast<float4*>(wo + ql * D + dd) = o4;
+        }
+      if (hi == 0) {
+        wo[128 * D + ql] = m_run;
+        wo[128 * D + 128 + ql] = l_tot;
+      }
     }
-    const float msc = -m_run * sl2;
-    float ps = 0.f;
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[mt][i], sl2, msc));
-        sacc[mt][i] = p;
-        ps += p;
-      }
-    l_run += ps;
-    bf16x8 pb[4];
-#pragma unroll
-    for (int kv = 0; kv < 4; ++kv)
-#pragma unroll
-      for (int i = 0; i < 8; ++i) pb[kv][i] = (bf16)sacc[kv >> 1][(kv & 1) * 8 + i];
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-      for (int kv = 0; kv < 4; ++kv) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&sV[cur][v_frag + dt * 32 * VR + kv * 16]);
-        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kv], oacc[dt], 0, 0, 0);
-      }
-    if (j + 1 < NT) sstore(cur ^ 1);
-    __syncthreads();
-  };
+  }
+}
 
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int j = 0; j < NT; j += 2) {
-    step(j, 0);
-    if (j + 1 < NT) step(j + 1, 1);
+// Combines the S pieces of each item in a fixed order (deterministic):
+// O = sum_p 2^((m_p - M) c) O_p / sum_p 2^((m_p - M) c) l_p, M = max_p m_p.
+// One workgroup per 32 queries of an item; a thread owns one query and 16
+// consecutive head dims.
+template <int D>
+__global__ __launch_bounds__(256) void attn_merge_kernel(bf16* __restrict__ O, int L, int H, int n_qt, int n_split,
+                                                         float sl2, const float* __restrict__ ws,
+                                                         const int* __restrict__ flag) {
+  if (flag != nullptr && *flag) return;
+  constexpr int TPQ = D / 16;  // threads per query
+  constexpr int QPB = 256 / TPQ;  // queries per workgroup
+  const int blocks_per_item = 128 / QPB;
+  const int item = blockIdx.x / blocks_per_item;
+  const int ql = (blockIdx.x % blocks_per_item) * QPB + threadIdx.x / TPQ;
+  const int d0 = (threadIdx.x % TPQ) * 16;
+  const int h = item / n_qt, qt = item - h * n_qt;
+  const int q = qt * 128 + ql;
+  if (q >= L) return;
+  const long long stride = 128 * D + 256;
+  const float* base = ws + (long long)item * n_split * stride;
+  float M = -INFINITY;
+  for (int p = 0; p < n_split; ++p) M = fmaxf(M, base[p * stride + 128 * D + ql]);
+  float acc[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) acc[i] = 0.f;
+  float den = 0.f;
+  for (int p = 0; p < n_split; ++p) {
+    const float* pp = base + p * stride;
+    const float w = __builtin_amdgcn_exp2f((pp[128 * D + ql] - M) * sl2);
+    den += w * pp[128 * D + 128 + ql];
+    const float4* src = reinterpret_cast<const float4*>(pp + ql * D + d0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float4 v = src[i];
+      acc[4 * i] += w * v.x;
+      acc[4 * i + 1] += w * v.y;
+      acc[4 * i + 2] += w * v.z;
+      acc[4 * i + 3] += w * v.w;
+    }
   }
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
-  const float inv = 1.0f / l_tot;
-  const int q = q0 + lo;
-  if (q < L) {
-    bf16* orow = O + (long long)q * C + h * D;
+  const float inv = 1.0f / den;
+  typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+  bf16x8 o0, o1;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int dd = dt * 32 + g * 8 + hi * 4;
-        typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-        bf16x4 o4;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) o4[r] = (bf16)(oacc[dt][g * 4 + r] * inv);
-        *reinterpret_cast<bf16x4*>(orow + dd) = o4;
-      }
+  for (int i = 0; i < 8; ++i) {
+    o0[i] = (bf16)(acc[i] * inv);
+    o1[i] = (bf16)(acc[8 + i] * inv);
   }
+  bf16* orow = O + (long long)q * H * D + h * D + d0;
+  *reinterpret_cast<bf16x8*>(orow) = o0;
+  *reinterpret_cast<bf16x8*>(orow + 8) = o1;
 }
 
 __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ Q, const float* __restrict__ Kc,
@@ -267,21 +446,68 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
 
 }  // namespace
 
+int resident_attention_groups() {
+  static int groups[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 512;
+  if (groups[dev] == 0) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) cus = 256;
+    groups[dev] = 2 * cus;
+  }
+  return groups[dev];
+}
+
+// Key splits per item.  Estimated time in key-tile steps of one resident
+// workgroup: rounds * (tiles per unit + 4 for the unit's prologue and
+// epilogue) + 4 S items / 512 for the merge, over S <= 4 with chunks of at
+// least 4 tiles (fitted to measured split sweeps on the multi-camera shapes).
+int attention_splits(int L, int Lk, int H) {
+  const int items = H * ((L + 127) / 128);
+  const int NT = (Lk + 63) / 64;
+  const int slots = resident_attention_groups();
+  int best = 1;
+  double best_cost = 1e300;
+  for (int s = 1; s <= 4 && (s == 1 || NT / s >= 4); ++s) {
+    const long long units = (long long)items * s;
+    const long long rounds = (units + slots - 1) / slots;
+    const double cost = (double)rounds * ((double)NT / s + 4.0) + (s > 1 ? 4.0 * s * items / 512.0 : 0.0);
+    if (cost < best_cost - 1e-9) {
+      best_cost = cost;
+      best = s;
+    }
+  }
+  return best;
+}
+
+size_t attention_workspace_floats(int L, int Lk, int H, int D) {
+  const int s = attention_splits(L, Lk, H);
+  if (s == 1) return 0;
+  return (size_t)H * ((L + 127) / 128) * s * (128 * (size_t)D + 256);
+}
+
 // bf16 requirements (checked by the caller): D in {64, 128}; Q has Mpad >=
-// roundup(L, 128) rows per head; the caches have Lcap >= roundup(Lk, 64) rows.
-void launch_attention(int dtype, const void* q, const void* kc, const void* vt, void* o, int L, int Mpad, int Lcap,
-                      int Lk, int H, int D, const int* flag, hipStream_t st) {
+// roundup(L, 128) rows per head; the caches have Lcap >= roundup(Lk, 64) rows
+// whose keys past Lk hold finite values; ws has
+// attention_workspace_floats(L, Lk, H, D) floats.
+void launch_attention(int dtype, const void* q, const void* kc, const void* vt, void* o, float* ws, int L, int Mpad,
+                      int Lcap, int Lk, int H, int D, const int* flag, hipStream_t st) {
   if (dtype == 1) {
     const int n_qt = (L + 127) / 128;
-    const int per_xcd = (H * n_qt + kXcds - 1) / kXcds;
-    const dim3 grid(per_xcd * kXcds);
+    const int n_split = attention_splits(L, Lk, H);
+    const int units = H * n_split * n_qt;
+    const int grid = (units + kXcds - 1) / kXcds * kXcds;
     const float sl2 = 1.4426950408889634f / sqrtf((float)D);
-    if (D == 128)
+    const int merge_grid = H * n_qt * (128 / (256 / (D / 16)));
+    if (D == 128) {
       attn_bf16_kernel<128><<<grid, 256, 0, st>>>((const bf16*)q, (const bf16*)kc, (const bf16*)vt, (bf16*)o, L,
-                                                  Mpad, Lcap, Lk, H, n_qt, sl2, flag);
-    else
+                                                  Mpad, Lcap, Lk, H, n_qt, n_split, sl2, ws, flag);
+      if (n_split > 1) attn_merge_kernel<128><<<merge_grid, 256, 0, st>>>((bf16*)o, L, H, n_qt, n_split, sl2, ws, flag);
+    } else {
       attn_bf16_kernel<64><<<grid, 256, 0, st>>>((const bf16*)q, (const bf16*)kc, (const bf16*)vt, (bf16*)o, L,
-                                                 Mpad, Lcap, Lk, H, n_qt, sl2, flag);
+                                                 Mpad, Lcap, Lk, H, n_qt, n_split, sl2, ws, flag);
+      if (n_split > 1) attn_merge_kernel<64><<<merge_grid, 256, 0, st>>>((bf16*)o, L, H, n_qt, n_split, sl2, ws, flag);
+    }
   } else {
     dim3 grid(L, H);
     attn_f32_kernel<<<grid, 64, 0, st>>>((const float*)q, (const float*)kc, (const float*)vt, (float*)o, L, Mpad,

@@ -64,6 +64,7 @@ struct xc_handle {
   void* hbuf = nullptr; float* qkv = nullptr; void* q = nullptr; void* o = nullptr; void* u = nullptr;
   float* x1 = nullptr; float* xa = nullptr; float* xb = nullptr;
   float* fp_partial = nullptr; double* fp_records = nullptr;
+  float* attn_ws = nullptr;
   // fingerprint tables
   FpTables tables{};
   int n_srows = 0, n_cams = 0, fp_rows = 0, n_wg = 0;
@@ -356,7 +357,8 @@ void compute_block(xc_handle* h, int b, const float* x, float* out, const int* f
   }
   {
     Prof p(h, XC_KERN_ATTENTION);
-    launch_attention(h->dtype, h->q, kc_b, vt_b, h->o, L, (int)h->Mpad, (int)h->Lcap, (int)Lk, H, D, flag, h->st);
+    launch_attention(h->dtype, h->q, kc_b, vt_b, h->o, h->attn_ws, L, (int)h->Mpad, (int)h->Lcap, (int)Lk, H, D, flag,
+                     h->st);
   }
   {
     Prof p(h, XC_KERN_GEMM_OPROJ);
@@ -573,6 +575,11 @@ void init_device(xc_handle* h, const float* w) {
   h->x1 = dalloc_t<float>(h, (size_t)h->L * C);
   h->xa = dalloc_t<float>(h, (size_t)h->L * C);
   h->xb = dalloc_t<float>(h, (size_t)h->L * C);
+  if (bf) {
+    size_t ws = 0;  // the key window grows chunk by chunk: size for the largest need
+    for (int w = 1; w <= h->Wkv; ++w) ws = std::max(ws, attention_workspace_floats((int)h->L, (int)(w * h->L), H, D));
+    if (ws) h->attn_ws = dalloc_t<float>(h, ws);
+  }
   // padded activation rows are read by the tile loads and must be finite
   XC_HIP(hipMemsetAsync(h->hbuf, 0, (size_t)h->Mpad * C * esz, h->st));
   XC_HIP(hipMemsetAsync(h->q, 0, (size_t)H * h->Mpad * D * esz, h->st));

@@ -92,8 +92,11 @@ void launch_gemm(int dtype, EpiMode mode, const void* A, const void* W, int M, i
 void launch_qk_norm(int dtype, const float* qkv, const float* gq, const float* gk, void* q, void* kring,
                     void* vtring, int L, int H, int D, int Mpad, int Lcap, int kv_off, const int* flag,
                     hipStream_t st);
-void launch_attention(int dtype, const void* q, const void* kring, const void* vtring, void* o, int L, int Mpad,
-                      int Lcap, int Lk, int H, int D, const int* flag, hipStream_t st);
+// Floats of the attention workspace (partials of items whose keys are split
+// across workgroups) for L queries over Lk keys, H heads of dimension D.
+size_t attention_workspace_floats(int L, int Lk, int H, int D);
+void launch_attention(int dtype, const void* q, const void* kring, const void* vtring, void* o, float* ws, int L,
+                      int Mpad, int Lcap, int Lk, int H, int D, const int* flag, hipStream_t st);
 void launch_skip_add(int dtype, const float* x, const void* rhat, float* out, long long n, const int* flag,
                      hipStream_t st);
 void launch_axpby(float a, const float* x, float b, const float* y, float* out, long long n, hipStream_t st);
