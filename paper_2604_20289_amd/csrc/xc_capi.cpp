@@ -14,8 +14,9 @@
 //   fingerprints   [S][B][n_srows + n_cams][C] float32
 //   gate state     EMA (NaN = unset), staleness, skip counts [S][B]; per-pass
 //                  skip flags and records [B]
-//   activations    h, q, o, u in the model dtype, padded to Mpad rows; the
-//                  float32 QKV staging buffer, x1 and two ping-pong streams.
+//   activations    h, q, o, u in the model dtype, padded to Mpad rows; x1
+//                  and two ping-pong streams (float32 models also stage the
+//                  QKV projection in float32 before the QK-norm kernel).
 //
 // One denoising pass enqueues, per block: for a gated block the fingerprint
 // reduction and the decision kernel (its flag stays on the device), then the
@@ -340,17 +341,36 @@ void compute_block(xc_handle* h, int b, const float* x, float* out, const int* f
     Prof p(h, XC_KERN_LN_MOD);
     launch_ln_mod(h->dtype, x, shift1, scale1, h->hbuf, L, C, flag, h->st);
   }
-  {
+  if (h->dtype == XC_BF16) {
+    // QKV projection with the per-head RMSNorm and the cache writes fused
     Prof p(h, XC_KERN_GEMM_QKV);
     EpiArgs e{};
     e.M = L;
     e.N = 3 * C;
     e.bias = h->bqkv + (size_t)b * 3 * C;
-    e.out_f32 = h->qkv;
-    launch_gemm(h->dtype, EPI_BIAS_F32, h->hbuf, wptr<void>(h->wqkv, (size_t)b * 3 * C * C, esz), L, 3 * C, C, e,
-                flag, h->st);
-  }
-  {
+    e.gq = h->gq + (size_t)b * D;
+    e.gk = h->gk + (size_t)b * D;
+    e.q_out = h->q;
+    e.k_cache = kc_b;
+    e.vt_cache = vt_b;
+    e.H = H;
+    e.D = D;
+    e.Mpad = (int)h->Mpad;
+    e.Lcap = (int)h->Lcap;
+    e.kv_off = (int)kv_off;
+    launch_gemm(h->dtype, EPI_QKV, h->hbuf, wptr<void>(h->wqkv, (size_t)b * 3 * C * C, esz), L, 3 * C, C, e, flag,
+                h->st);
+  } else {
+    {
+      Prof p(h, XC_KERN_GEMM_QKV);
+      EpiArgs e{};
+      e.M = L;
+      e.N = 3 * C;
+      e.bias = h->bqkv + (size_t)b * 3 * C;
+      e.out_f32 = h->qkv;
+      launch_gemm(h->dtype, EPI_BIAS_F32, h->hbuf, wptr<void>(h->wqkv, (size_t)b * 3 * C * C, esz), L, 3 * C, C, e,
+                  flag, h->st);
+    }
     Prof p(h, XC_KERN_QK_NORM);
     launch_qk_norm(h->dtype, h->qkv, h->gq + (size_t)b * D, h->gk + (size_t)b * D, h->q, kc_b, vt_b, L, H, D,
                    (int)h->Mpad, (int)h->Lcap, (int)kv_off, flag, h->st);
@@ -568,7 +588,7 @@ void init_device(xc_handle* h, const float* w) {
   h->cond = dalloc_t<float>(h, kMaxCond);
   h->mod = dalloc_t<float>(h, (size_t)B * 6 * C);
   h->hbuf = dalloc(h, (size_t)h->Mpad * C * esz);
-  h->qkv = dalloc_t<float>(h, (size_t)h->Mpad * 3 * C);
+  if (!bf) h->qkv = dalloc_t<float>(h, (size_t)h->Mpad * 3 * C);
   h->q = dalloc(h, (size_t)H * h->Mpad * D * esz);
   h->o = dalloc(h, (size_t)h->Mpad * C * esz);
   h->u = dalloc(h, (size_t)h->Mpad * Dm * esz);
@@ -657,7 +677,9 @@ xc_status xc_init(const xc_model_config* model, const xc_gate_config* gate, cons
   h->dtype = model->dtype;
   h->esz = model->dtype == XC_BF16 ? 2 : 4;
   h->L = tokens_of(model);
-  h->Mpad = (h->L + 255) / 256 * 256;
+  // activation rows padded for every GEMM tile height (128, 192, 256) and the
+  // 128-query attention tiles: roundup(L, 256) + 256 >= roundup(L, 192)
+  h->Mpad = (h->L + 255) / 256 * 256 + 256;
   h->Lcap = ((long long)h->Wkv * h->L + 63) / 64 * 64;
   try {
     XC_HIP(hipGetDevice(&h->device));

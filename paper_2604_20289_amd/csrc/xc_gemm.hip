@@ -45,7 +45,7 @@ __device__ __forceinline__ void epilogue(const EpiArgs& e, int m, int n, float a
     e.out_f32[i] = e.resid[i] + e.gate[n] * v;
   } else if constexpr (MODE == EPI_UP) {
     reinterpret_cast<T*>(e.out_t)[i] = cvt<T>(gelu_tanh(v));
-  } else {
+  } else if constexpr (MODE == EPI_DOWN) {
     const float xin = e.xin[i];
     const float y = e.resid[i] + e.gate[n] * v;
     e.out_f32[i] = y;
@@ -53,92 +53,254 @@ __device__ __forceinline__ void epilogue(const EpiArgs& e, int m, int n, float a
   }
 }
 
-constexpr int BM = 128, BN = 128, BK = 64;
+// ---------------------------------------------------------------------------
+// bf16 MFMA GEMM.  Workgroup = 4 waves in a 2x2 arrangement; a wave owns an
+// (MT*32) x (NT*32) sub-tile, i.e. MT x NT independent 32x32 accumulators of
+// v_mfma_f32_32x32x16_bf16, so each 16-byte LDS fragment feeds several
+// MFMAs.  K advances 32 per stage; the A and B stage tiles (64-byte rows) go
+// from global memory straight into a 3-stage LDS ring (no staging
+// registers, no LDS store instructions), two stages ahead of the MFMAs, and
+// their 16-byte chunks are XOR-swizzled by (row / 4) so the rows a half-wave
+// reads fall in distinct banks.  The 1-D grid is dealt to the XCDs in
+// contiguous ranges of tiles, ordered in groups of 8 M-tiles x all N-tiles
+// so concurrently resident tiles share A row blocks and B column blocks in
+// the XCD's L2.
+// ---------------------------------------------------------------------------
+constexpr int kXcd = 8;
+constexpr int GBK = 32;
 
-__device__ __forceinline__ int swz(int row, int kc) { return row * BK + ((kc ^ (row & 7)) << 3); }
+template <int MT, int NT>
+struct GemmTile {
+  static constexpr int BM = 2 * MT * 32, BN = 2 * NT * 32;
+  static constexpr int A_PER_T = BM * 4 / 256, B_PER_T = BN * 4 / 256;  // 16-byte chunks per thread and stage
+  static constexpr int STAGE = (BM + BN) * GBK;                         // bf16 elements per stage
+};
 
-template <int MODE>
+__device__ __forceinline__ int swz32(int row, int c) { return row * GBK + ((c ^ ((row >> 2) & 3)) << 3); }
+
+// LDS bytes of the QKV epilogue: row sums of squares [BM][65] floats, reused
+// as the V^T transpose buffer [BN][BM + 8] bf16.
+template <int MT, int NT>
+constexpr int qkv_epi_bytes() {
+  return GemmTile<MT, NT>::BM * 65 * 4 > GemmTile<MT, NT>::BN * (GemmTile<MT, NT>::BM + 8) * 2
+             ? GemmTile<MT, NT>::BM * 65 * 4
+             : GemmTile<MT, NT>::BN * (GemmTile<MT, NT>::BM + 8) * 2;
+}
+
+template <int MODE, int MT, int NT>
 __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(const bf16* __restrict__ A, const bf16* __restrict__ W,
                                                            int M, int N, int K, EpiArgs e,
                                                            const int* __restrict__ flag) {
   if (flag != nullptr && *flag) return;
-  __shared__ __attribute__((aligned(16))) bf16 sA[2][BM * BK];
-  __shared__ __attribute__((aligned(16))) bf16 sB[2][BN * BK];
+  typedef GemmTile<MT, NT> T;
+  constexpr int MAIN_BYTES = 3 * T::STAGE * 2;
+  constexpr int EPI_BYTES = MODE == EPI_QKV ? qkv_epi_bytes<MT, NT>() : 0;
+  constexpr int LDS_BYTES = MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES;
+  __shared__ __attribute__((aligned(16))) char lds[LDS_BYTES];
+  bf16* sbuf = reinterpret_cast<bf16*>(lds);
+
+  const int n_tm = (M + T::BM - 1) / T::BM, n_tn = N / T::BN;
+  const int total = n_tm * n_tn;
+  const int per_xcd = (total + kXcd - 1) / kXcd;
+  const int t = (blockIdx.x % kXcd) * per_xcd + blockIdx.x / kXcd;
+  if (t >= total) return;
+  constexpr int GM = 8;
+  const int in_group = GM * n_tn;
+  const int first_m = (t / in_group) * GM;
+  const int gm = min(GM, n_tm - first_m);
+  const int tm = first_m + (t % in_group) % gm, tn = (t % in_group) / gm;
+  const int m0 = tm * T::BM, n0 = tn * T::BN;
+
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const int hi = lane >> 5, lo = lane & 31;
   const bf16* Ab = A + (long long)m0 * K;
   const bf16* Wb = W + (long long)n0 * K;
-  u32x4 ra[4], rb[4];
-  f32x16 acc[2][2];
+  f32x16 acc[MT][NT];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < MT; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < NT; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  const int KT = K / BK;
-  auto gload = [&](int kt) __attribute__((always_inline)) {
+  const int KT = K / GBK;
+  // Stages go global -> LDS directly (global_load_lds_dwordx4): one wave
+  // instruction fills 1 KB of LDS lane-linearly, i.e. 16 rows x 4 chunks; a
+  // lane fetches the logical chunk that the swizzle places at its position.
+  constexpr int A_INSTR = T::BM / 16 / 4, B_INSTR = T::BN / 16 / 4;  // per wave
+  constexpr int LOADS = A_INSTR + B_INSTR;
+  const int lrow = lane >> 2, lpc = lane & 3;
+  auto issue = [&](int kt, int buf) __attribute__((always_inline)) {
+    bf16* sa = sbuf + buf * T::STAGE;
+    bf16* sb = sa + T::BM * GBK;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int q = tid + 256 * i, row = q >> 3, kc = q & 7;
-      ra[i] = *reinterpret_cast<const u32x4*>(Ab + (long long)row * K + kt * BK + kc * 8);
-      rb[i] = *reinterpret_cast<const u32x4*>(Wb + (long long)row * K + kt * BK + kc * 8);
+    for (int i = 0; i < A_INSTR; ++i) {
+      const int I = wave + 4 * i, row = I * 16 + lrow, c = lpc ^ ((row >> 2) & 3);
+      __builtin_amdgcn_global_load_lds(Ab + (long long)row * K + kt * GBK + c * 8, sa + I * 512, 16, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < B_INSTR; ++i) {
+      const int I = wave + 4 * i, row = I * 16 + lrow, c = lpc ^ ((row >> 2) & 3);
+      __builtin_amdgcn_global_load_lds(Wb + (long long)row * K + kt * GBK + c * 8, sb + I * 512, 16, 0, 0);
     }
   };
-  auto sstore = [&](int buf) __attribute__((always_inline)) {
+  auto compute = [&](int buf) __attribute__((always_inline)) {
+    const bf16* sa = sbuf + buf * T::STAGE;
+    const bf16* sb = sa + T::BM * GBK;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int q = tid + 256 * i, row = q >> 3, kc = q & 7;
-      *reinterpret_cast<u32x4*>(&sA[buf][swz(row, kc)]) = ra[i];
-      *reinterpret_cast<u32x4*>(&sB[buf][swz(row, kc)]) = rb[i];
-    }
-  };
-
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < KT; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < KT) gload(kt + 1);
+    for (int kk = 0; kk < GBK / 16; ++kk) {
+      const int c = kk * 2 + hi;
+      bf16x8 a[MT], b[NT];
 #pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      const int kc = kk * 2 + (lane >> 5);
-      bf16x8 a[2], b[2];
+      for (int mt = 0; mt < MT; ++mt) a[mt] = *reinterpret_cast<const bf16x8*>(&sa[swz32(wm * MT * 32 + mt * 32 + lo, c)]);
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt) {
-        const int row = wm * 64 + mt * 32 + (lane & 31);
-        a[mt] = *reinterpret_cast<const bf16x8*>(&sA[cur][swz(row, kc)]);
-      }
+      for (int nt = 0; nt < NT; ++nt) b[nt] = *reinterpret_cast<const bf16x8*>(&sb[swz32(wn * NT * 32 + nt * 32 + lo, c)]);
 #pragma unroll
-      for (int nt = 0; nt < 2; ++nt) {
-        const int row = wn * 64 + nt * 32 + (lane & 31);
-        b[nt] = *reinterpret_cast<const bf16x8*>(&sB[cur][swz(row, kc)]);
-      }
+      for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt)
+        for (int nt = 0; nt < NT; ++nt)
           acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mt], b[nt], acc[mt][nt], 0, 0, 0);
     }
-    if (kt + 1 < KT) sstore(cur ^ 1);
-    __syncthreads();
-  }
+  };
+  // vmcnt(n) with the other counters left at their maximum (gfx9 encoding)
+#define XC_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt((0x3f70) | ((n) & 15) | (((n) >> 4) << 14))
 
-  // accumulator element (g, r) of a 32x32 block: row g*8 + (lane/32)*4 + r, column lane%32
+  // Stage k lives in LDS buffer k mod 3; stage k+2 is requested while stage k
+  // is multiplied, and stage k+1 (requested one step earlier) is waited for
+  // before the barrier.  Requests past the last stage repeat it (in bounds,
+  // into a buffer nobody reads again), so every step is the same code.
+  issue(0, 0);
+  issue(min(1, KT - 1), 1);
+  XC_WAIT_VMCNT(LOADS);
+  __syncthreads();
+  auto step = [&](int kt, int b0, int b2) __attribute__((always_inline)) {  // b0 = kt mod 3, b2 = (kt+2) mod 3
+    issue(min(kt + 2, KT - 1), b2);
+    compute(b0);
+    XC_WAIT_VMCNT(LOADS);
+    __syncthreads();
+  };
+  int kt = 0;
+  for (; kt + 2 < KT; kt += 3) {
+    step(kt, 0, 2);
+    step(kt + 1, 1, 0);
+    step(kt + 2, 2, 1);
+  }
+  if (kt < KT) step(kt, 0, 2);
+  if (kt + 1 < KT) step(kt + 1, 1, 0);
+  XC_WAIT_VMCNT(0);  // the epilogue may reuse the LDS: no request may still be landing
+  __syncthreads();
+#undef XC_WAIT_VMCNT
+
+  // accumulator element (mt, nt, g, r): tile row wm*MT*32 + mt*32 + g*8 + hi*4 + r,
+  // tile column wn*NT*32 + nt*32 + lo
+  if constexpr (MODE == EPI_QKV) {
+    const int C = e.H * e.D;
+    const int part = n0 / C;  // 0 q, 1 k, 2 v (a tile never straddles two parts)
+    const int head0 = (n0 - part * C) / e.D;
 #pragma unroll
-  for (int mt = 0; mt < 2; ++mt)
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt)
+      for (int nt = 0; nt < NT; ++nt) {
+        const float bv = e.bias[n0 + wn * NT * 32 + nt * 32 + lo];
 #pragma unroll
-      for (int g = 0; g < 4; ++g)
+        for (int r = 0; r < 16; ++r) acc[mt][nt][r] += bv;
+      }
+    if (part < 2) {
+      // per (row, head) RMS over the head's D columns: lane partials -> LDS
+      float* ss = reinterpret_cast<float*>(lds);  // [BM][65]
+      const int slot = wn * 32 + lo;             // 64 column slots of 2 columns' squares each
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = m0 + wm * 64 + mt * 32 + g * 8 + (lane >> 5) * 4 + r;
-          const int col = n0 + wn * 64 + nt * 32 + (lane & 31);
-          if (row < M) epilogue<MODE, bf16>(e, row, col, acc[mt][nt][g * 4 + r]);
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            float p = 0.f;
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) p += acc[mt][nt][g * 4 + r] * acc[mt][nt][g * 4 + r];
+            ss[(wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r) * 65 + slot] = p;
+          }
+      __syncthreads();
+      // heads per tile: 128 / D (1 for D = 128, 2 for D = 64); slots per head 64 / heads
+      const int hpt = T::BN / e.D, sph = 64 / hpt;
+      for (int idx = tid; idx < T::BM * hpt; idx += 256) {
+        const int row = idx / hpt, hd = idx - row * hpt;
+        float sum = 0.f;
+        for (int j = 0; j < sph; ++j) sum += ss[row * 65 + hd * sph + j];
+        ss[row * 65 + 64 - hd] = 1.0f / sqrtf(sum / (float)e.D + 1e-6f);  // slots 64, 63 hold the scales
+      }
+      __syncthreads();
+      const float* gain = part == 0 ? e.gq : e.gk;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int trow = wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r;
+            const int row = m0 + trow;
+            if (row >= M) continue;
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+              const int tcol = wn * NT * 32 + nt * 32 + lo;
+              const int hd = tcol / e.D, dd = tcol - hd * e.D;
+              const float v = acc[mt][nt][g * 4 + r] * ss[trow * 65 + 64 - hd] * gain[dd];
+              const long long hh = head0 + hd;
+              bf16* dst = part == 0 ? reinterpret_cast<bf16*>(e.q_out) + (hh * e.Mpad + row) * e.D + dd
+                                    : reinterpret_cast<bf16*>(e.k_cache) + (hh * e.Lcap + e.kv_off + row) * e.D + dd;
+              *dst = (bf16)v;
+            }
+          }
+    } else {
+      // V^T: transpose the tile through LDS, then write rows of consecutive tokens
+      bf16* vt = reinterpret_cast<bf16*>(lds);  // [BN][BM + 8]
+      constexpr int VS = T::BM + 8;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+          for (int g = 0; g < 4; ++g)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              vt[(wn * NT * 32 + nt * 32 + lo) * VS + wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r] =
+                  (bf16)acc[mt][nt][g * 4 + r];
+      __syncthreads();
+      const int rows = min(T::BM, M - m0);
+      for (int idx = tid; idx < T::BN * (T::BM / 2); idx += 256) {
+        const int col = idx / (T::BM / 2), rp = (idx - col * (T::BM / 2)) * 2;
+        if (rp >= rows) continue;
+        const int hd = col / e.D, dd = col - hd * e.D;
+        bf16* dst = reinterpret_cast<bf16*>(e.vt_cache) + ((long long)(head0 + hd) * e.D + dd) * e.Lcap + e.kv_off + m0 + rp;
+        if (rp + 1 < rows) {
+          typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+          bf16x2 two = {vt[col * VS + rp], vt[col * VS + rp + 1]};
+          if (((e.kv_off + m0 + rp) & 1) == 0) {
+            *reinterpret_cast<bf16x2*>(dst) = two;
+          } else {
+            dst[0] = two[0];
+            dst[1] = two[1];
+          }
+        } else {
+          dst[0] = vt[col * VS + rp];
         }
+      }
+    }
+  } else {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int row = m0 + wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r;
+            const int col = n0 + wn * NT * 32 + nt * 32 + lo;
+            if (row < M) epilogue<MODE, bf16>(e, row, col, acc[mt][nt][g * 4 + r]);
+          }
+  }
 }
 
 template <int MODE>
@@ -182,12 +344,48 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
     }
 }
 
+// Rows per M-tile for an M x N product: the tile height (64*MT) whose tile
+// count best fills whole rounds of resident workgroups (2 per CU).
+int pick_mt(int M, int N) {
+  static int slots = 0;
+  if (slots == 0) {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+      cus = 256;
+    slots = 2 * cus;
+  }
+  int best = 4;
+  double best_cost = 1e300;
+  for (int mt = 4; mt >= 2; --mt) {
+    const long long tiles = (long long)((M + 64 * mt - 1) / (64 * mt)) * (N / 128);
+    const long long rounds = (tiles + slots - 1) / slots;
+    const double cost = (double)rounds * mt;  // one round costs in proportion to the tile height
+    if (cost < best_cost - 1e-9) {
+      best_cost = cost;
+      best = mt;
+    }
+  }
+  return best;
+}
+
+template <int MODE, int MT>
+void launch_bf16(const void* A, const void* W, int M, int N, int K, const EpiArgs& e, const int* flag, hipStream_t st) {
+  typedef GemmTile<MT, 2> T;
+  const int tiles = ((M + T::BM - 1) / T::BM) * (N / T::BN);
+  const int grid = (tiles + kXcd - 1) / kXcd * kXcd;
+  gemm_bf16_kernel<MODE, MT, 2><<<grid, 256, 0, st>>>((const bf16*)A, (const bf16*)W, M, N, K, e, flag);
+}
+
 template <int MODE>
 void launch_mode(int dtype, const void* A, const void* W, int M, int N, int K, const EpiArgs& e, const int* flag,
                  hipStream_t st) {
   if (dtype == 1) {
-    dim3 grid(N / BN, (M + BM - 1) / BM);
-    gemm_bf16_kernel<MODE><<<grid, 256, 0, st>>>((const bf16*)A, (const bf16*)W, M, N, K, e, flag);
+    switch (pick_mt(M, N)) {
+      case 4: launch_bf16<MODE, 4>(A, W, M, N, K, e, flag, st); break;
+      case 3: launch_bf16<MODE, 3>(A, W, M, N, K, e, flag, st); break;
+      default: launch_bf16<MODE, 2>(A, W, M, N, K, e, flag, st); break;
+    }
   } else {
     dim3 grid((N + 63) / 64, (M + 63) / 64);
     gemm_f32_kernel<MODE><<<grid, 256, 0, st>>>((const float*)A, (const float*)W, M, N, K, e, flag);
@@ -196,8 +394,9 @@ void launch_mode(int dtype, const void* A, const void* W, int M, int N, int K, c
 
 }  // namespace
 
-// bf16 requirements (checked by the caller): N % 128 == 0, K % 64 == 0, A has
-// at least roundup(M, 128) rows allocated.
+// bf16 requirements (checked by the caller): N % 128 == 0, K % 32 == 0, A has
+// at least roundup(M, 256) rows allocated; EPI_QKV needs C % 128 == 0 and
+// D in {64, 128}.
 void launch_gemm(int dtype, EpiMode mode, const void* A, const void* W, int M, int N, int K, const EpiArgs& e,
                  const int* flag, hipStream_t st) {
   switch (mode) {
@@ -205,6 +404,7 @@ void launch_gemm(int dtype, EpiMode mode, const void* A, const void* W, int M, i
     case EPI_OPROJ: launch_mode<EPI_OPROJ>(dtype, A, W, M, N, K, e, flag, st); break;
     case EPI_UP: launch_mode<EPI_UP>(dtype, A, W, M, N, K, e, flag, st); break;
     case EPI_DOWN: launch_mode<EPI_DOWN>(dtype, A, W, M, N, K, e, flag, st); break;
+    case EPI_QKV: launch_mode<EPI_QKV>(dtype, A, W, M, N, K, e, flag, st); break;
   }
 }
 

@@ -27,6 +27,7 @@ enum EpiMode : int {
   EPI_OPROJ = 1,     // out_f32 = resid + gate * (acc + bias)          (x1)
   EPI_UP = 2,        // out_t  = gelu_tanh(acc + bias)                   (u)
   EPI_DOWN = 3,      // out_f32 = resid + gate * (acc + bias)  (y); out_t = y - xin (cached residual)
+  EPI_QKV = 4,       // acc + bias; per-head RMSNorm * gain on q and k; q -> q_out, k/v -> caches (bf16)
 };
 
 struct EpiArgs {
@@ -38,6 +39,13 @@ struct EpiArgs {
   const float* resid;  // [M][N]
   const float* gate;   // [N]
   const float* xin;    // [M][N]
+  // EPI_QKV: columns [0, C) are q, [C, 2C) k, [2C, 3C) v, C = H * D
+  const float* gq;     // [D]
+  const float* gk;     // [D]
+  void* q_out;         // [H][Mpad][D]
+  void* k_cache;       // [H][Lcap][D], token m at row kv_off + m
+  void* vt_cache;      // [H][D][Lcap], token m at column kv_off + m
+  int H, D, Mpad, Lcap, kv_off;
 };
 
 // Per-pass gate hyper-parameters handed to the decision kernel.
