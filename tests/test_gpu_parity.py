@@ -186,3 +186,45 @@ def test_determinism_bf16():
         xc.close()
     for a, b in zip(*runs):
         np.testing.assert_array_equal(a, b)
+
+
+DEGENERATE = {
+    # one block, no anchors: the only block is gated
+    "one-block-no-anchor": synth.with_stream(synth.with_model(
+        synth.with_gate(W0, adaptive=1, tau_floor=0.9, tau_dev=2.0, front_anchors=0), n_blocks=1), rho=0.999),
+    # a single denoising step per chunk
+    "one-step": synth.with_stream(synth.with_model(
+        synth.with_gate(W0, adaptive=1, tau_floor=0.9, tau_dev=2.0), n_steps=1), rho=0.999),
+    # every block an anchor: nothing is ever gated
+    "all-anchors": synth.with_gate(W0, adaptive=1, tau_floor=0.9, tau_dev=2.0, front_anchors=1, back_anchors=1),
+    # warmup of two generations and a longer window than the stream
+    "warmup2-window4": synth.with_stream(synth.with_model(
+        synth.with_gate(W0, adaptive=1, tau_floor=0.9, tau_dev=2.0, warmup=2), kv_window=4), rho=0.999),
+}
+
+
+@pytest.mark.parametrize("name", list(DEGENERATE))
+def test_degenerate_configs(name):
+    ls = _ls(DEGENERATE[name])
+    try:
+        st = ls.run(5, tol_abs=TOL32)
+        if name == "all-anchors":
+            assert st["gated_evals"] == 0 and st["skips"] == 0
+    finally:
+        ls.close()
+
+
+def test_bf16_three_view_groups():
+    """Three view groups with different grids (front/side/rear-like), one back anchor."""
+    w = synth.Workload(
+        "bf16-three-groups",
+        synth.ModelShape(3, 256, 4, 64, 512, 256, 16, synth.BF16, 4, 2,
+                         (synth.ViewGroup(2, 2, 6, 10), synth.ViewGroup(3, 2, 4, 7), synth.ViewGroup(1, 3, 5, 5))),
+        synth.GateParams(back_anchors=1),
+        synth.StreamParams(4, 0.999, 0.02),
+    )
+    ls = _ls(w)
+    try:
+        ls.run(4, tol_rel_l2=TOLBF)
+    finally:
+        ls.close()
