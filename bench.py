@@ -43,12 +43,13 @@ METRIC = "chunk latency ms + block TFLOP/s vs MFMA peak + block skip rate, 1 GPU
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 
-# HBM-side bytes per full-window attention launch from the rocprofv3 FETCH_SIZE
-# and WRITE_SIZE passes (scaled by a 512 MiB copy-kernel calibration), valid
-# only for the kernel source they were taken on (sha1 prefix of the file).
+# HBM-side bytes per full-window attention op (main dispatch + merge of the
+# key-split partials) from the rocprofv3 FETCH_SIZE and WRITE_SIZE passes,
+# scaled by a 512 MiB copy-kernel calibration; valid only for the kernel
+# source they were taken on (sha1 prefix of the file).
 MEASURED_TRAFFIC = {
-    "attention": {"source": "paper_2604_20289_amd/csrc/xc_attention.hip", "sha1": "c784234d81e95e0c",
-                  "bytes": (316.3 + 21.6) * 1e6},
+    "attention": {"source": "paper_2604_20289_amd/csrc/xc_attention.hip", "sha1": "a39a672cb825f0fd",
+                  "bytes": (523.8 + 153.4) * 1e6},
 }
 
 
