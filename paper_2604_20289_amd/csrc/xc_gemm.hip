@@ -1,13 +1,16 @@
 // Dense projections of the DiT block: C[M][N] = A[M][K] * W[N][K]^T with fused
-// epilogues (bias, gated residual, tanh-GELU, cached-residual store).
+// epilogues (bias, gated residual, tanh-GELU, cached-residual store, and for
+// the QKV projection the per-head RMSNorm with the K / V^T cache stores).
 //
-// bf16 path: 128x128x64 workgroup tiles, 4 waves in a 2x2 arrangement, each
-// wave a 64x64 sub-tile of 2x2 v_mfma_f32_32x32x16_bf16 blocks with float
+// bf16 path, two kernels built on v_mfma_f32_32x32x16_bf16 with float
 // accumulation.  Both operands are K-contiguous (activations row-major,
-// weights [out][in]), so a lane's MFMA operand is one 16-byte LDS read.  LDS
-// tiles are double-buffered (global loads of tile k+1 are in flight while
-// tile k is multiplied) and their 16-byte chunks are XOR-swizzled by row so
-// the 32 rows a half-wave reads hit distinct banks.
+// weights [out][in]), so a lane's MFMA operand is one 16-byte LDS read, and
+// stage tiles go from global memory straight into LDS (global_load_lds).
+//  * gemm_bf16_kernel: (64*MT) x 128 tiles, two workgroups per CU; used for
+//    the fused QKV projection and for widths that are not multiples of 192.
+//  * gemm_bf16_persistent: 256 x 192 tiles, one persistent workgroup per CU
+//    streaming its tiles through a 4-deep LDS ring; used for the other
+//    projections.
 //
 // fp32 path: a plain LDS-tiled FMA GEMM (64x64 tiles, 4x4 per thread) used
 // for float32 models.
@@ -303,6 +306,283 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(const bf16* __restric
   }
 }
 
+// ---------------------------------------------------------------------------
+// Persistent bf16 MFMA GEMM for the large products.  One workgroup of 4 waves
+// per CU (the grid never exceeds the CU count); a workgroup owns a 256 x BN
+// output tile (BN = 64*NT) per turn, its waves in a 2x2 arrangement of
+// 128 x (32*NT) sub-tiles held as 4 x NT accumulators (in AGPRs).  Per output
+// element this needs a third less operand traffic from L2 than two resident
+// 256 x 128 workgroups.  A workgroup walks its tiles as one continuous stream
+// of K=32 stages through a 4-deep LDS ring filled straight from global memory
+// (global_load_lds_dwordx4) three stages ahead, so the first stages of the next
+// tile load while the current tile finishes and runs its epilogue.  The MFMA
+// operands of the next 16-wide K slice are read from LDS while the current
+// slice's MFMAs issue.  Tiles are dealt to workgroups in the grouped order
+// (8 M-tiles x all N-tiles), each XCD taking a contiguous range per turn.
+// Used for the element-wise epilogues; K must be a multiple of 128.
+// ---------------------------------------------------------------------------
+constexpr int PBM = 256;
+constexpr int PNB = 4;
+
+template <int NT>
+struct PTile {
+  static constexpr int BN = 64 * NT;
+  static constexpr int STAGE = (PBM + BN) * GBK;                 // bf16 elements per stage
+  static constexpr int A_INSTR = PBM / 64, B_INSTR = BN / 64;   // load instructions per wave and stage
+  static constexpr int LOADS = A_INSTR + B_INSTR;
+};
+
+__device__ __forceinline__ void grouped_tile(int j, int n_tm, int n_tn, int& tm, int& tn) {
+  constexpr int GM = 8;
+  const int in_group = GM * n_tn;
+  const int first_m = (j / in_group) * GM;
+  const int gm = min(GM, n_tm - first_m);
+  tm = first_m + (j % in_group) % gm;
+  tn = (j % in_group) / gm;
+}
+
+// Epilogue of the persistent kernel for the element-wise modes.  The lane's
+// rows are r0 + mt*32 + g*8 + r, its columns cb + nt*32.  Column constants
+// (bias, gate) are read once; each row's operand loads are issued together
+// before its stores; rows past M are never stored (their loads use a clamped
+// row).  Blocks of 4 rows are processed one at a time, which bounds the live
+// registers.
+template <int MODE, int NT>
+__device__ __forceinline__ void persistent_epilogue(const EpiArgs& e, const f32x16 (&acc)[4][NT], int r0, int cb,
+                                                    int M) {
+  float bias[NT], gate[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    bias[nt] = e.bias[cb + nt * 32];
+    gate[nt] = (MODE == EPI_OPROJ || MODE == EPI_DOWN) ? e.gate[cb + nt * 32] : 0.f;
+  }
+  const long long N = e.N;
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      // this block's 4 x NT accumulators move to VGPRs here, not all at once
+      float v[4][NT];
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          v[r][nt] = acc[mt][nt][g * 4 + r];
+          asm volatile("" : "+v"(v[r][nt]));
+        }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = r0 + mt * 32 + g * 8 + r;
+        const long long il = (long long)min(row, M - 1) * N + cb;
+        const long long is = (long long)row * N + cb;
+        float res[NT], xin[NT];
+        if constexpr (MODE == EPI_OPROJ || MODE == EPI_DOWN) {
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) res[nt] = e.resid[il + nt * 32];
+        }
+        if constexpr (MODE == EPI_DOWN) {
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) xin[nt] = e.xin[il + nt * 32];
+        }
+        if (row >= M) continue;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const float x = v[r][nt] + bias[nt];
+          if constexpr (MODE == EPI_BIAS_F32) {
+            e.out_f32[is + nt * 32] = x;
+          } else if constexpr (MODE == EPI_OPROJ) {
+            e.out_f32[is + nt * 32] = res[nt] + gate[nt] * x;
+          } else if constexpr (MODE == EPI_UP) {
+            reinterpret_cast<bf16*>(e.out_t)[is + nt * 32] = (bf16)gelu_tanh(x);
+          } else if constexpr (MODE == EPI_DOWN) {
+            const float y = res[nt] + gate[nt] * x;
+            e.out_f32[is + nt * 32] = y;
+            if (e.out_t != nullptr) reinterpret_cast<bf16*>(e.out_t)[is + nt * 32] = (bf16)(y - xin[nt]);
+          }
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
+// vmcnt(n) lgkmcnt(0) (gfx9 encoding, expcnt left at its maximum)
+#define XC_WAIT_VM_LGKM0(n) __builtin_amdgcn_s_waitcnt(0x0070 | ((n) & 15) | (((n) >> 4) << 14))
+
+template <int MODE, int NT>
+__global__ __launch_bounds__(256, 1) void gemm_bf16_persistent(const bf16* __restrict__ A,
+                                                               const bf16* __restrict__ W, int M, int N, int K,
+                                                               EpiArgs e, const int* __restrict__ flag) {
+  if (flag != nullptr && *flag) return;
+  typedef PTile<NT> T;
+  // One LDS array per ring slot (slot = stage mod 4, a constant at every use
+  // after unrolling): the compiler then tracks which slot each LDS-DMA request
+  // writes and does not hold reads of other slots behind it.
+  __shared__ __attribute__((aligned(16))) bf16 stg0[T::STAGE];
+  __shared__ __attribute__((aligned(16))) bf16 stg1[T::STAGE];
+  __shared__ __attribute__((aligned(16))) bf16 stg2[T::STAGE];
+  __shared__ __attribute__((aligned(16))) bf16 stg3[T::STAGE];
+  auto stage = [&](int b) __attribute__((always_inline)) -> bf16* {
+    return b == 0 ? stg0 : (b == 1 ? stg1 : (b == 2 ? stg2 : stg3));
+  };
+
+  const int n_tm = (M + PBM - 1) / PBM, n_tn = N / T::BN, n_tiles = n_tm * n_tn;
+  const int G = gridDim.x;
+  const int slot = (G % kXcd == 0) ? (blockIdx.x % kXcd) * (G / kXcd) + blockIdx.x / kXcd : blockIdx.x;
+  if (slot >= n_tiles) return;
+  const int n_my = (n_tiles - 1 - slot) / G + 1;
+  const int KT = K / GBK;
+  const int n_stages = n_my * KT;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int hi = lane >> 5, lo = lane & 31;
+  // A load instruction i of this wave fills stage rows (wave + 4i)*16 .. +15,
+  // lane-linearly: the lane's 16 bytes land at row (lane/4), physical chunk
+  // lane%4, which holds logical chunk (lane%4) ^ ((row/4)%4).
+  const int lrow = lane >> 2, lchunk = (lane & 3) ^ ((lrow >> 2) & 3);
+  const int ld_off = lrow * K + lchunk * 8;  // + (wave + 4i) * 16 * K
+
+  // Loader state: the next stage to request (its tile and K step).  Past the
+  // last stage the requests repeat it (in bounds, into a buffer that is never
+  // read), so every step of the loop is the same code.
+  int ld_i = 0, ld_kt = 0;
+  const bf16* ldA;
+  const bf16* ldW;
+  auto ld_tile = [&](int i) __attribute__((always_inline)) {
+    int tm, tn;
+    grouped_tile(slot + i * G, n_tm, n_tn, tm, tn);
+    ldA = A + (long long)tm * PBM * K + ld_off;
+    ldW = W + (long long)tn * T::BN * K + ld_off;
+  };
+  ld_tile(0);
+  auto issue = [&](int buf) __attribute__((always_inline)) {
+    bf16* sa = stage(buf);
+    bf16* sb = sa + PBM * GBK;
+#pragma unroll
+    for (int j = 0; j < T::A_INSTR; ++j)
+      __builtin_amdgcn_global_load_lds(ldA + (long long)(wave + 4 * j) * 16 * K, sa + (wave + 4 * j) * 512, 16, 0, 0);
+#pragma unroll
+    for (int j = 0; j < T::B_INSTR; ++j)
+      __builtin_amdgcn_global_load_lds(ldW + (long long)(wave + 4 * j) * 16 * K, sb + (wave + 4 * j) * 512, 16, 0, 0);
+    if (ld_kt + 1 < KT) {
+      ++ld_kt;
+      ldA += GBK;
+      ldW += GBK;
+    } else if (ld_i + 1 < n_my) {
+      ld_kt = 0;
+      ld_tile(++ld_i);
+    }
+  };
+  auto frags = [&](int buf, int kk, bf16x8* a, bf16x8* b) __attribute__((always_inline)) {
+    const bf16* sa = stage(buf);
+    const bf16* sb = sa + PBM * GBK;
+    const int c = kk * 2 + hi;
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) a[mt] = *reinterpret_cast<const bf16x8*>(&sa[swz32(wm * 128 + mt * 32 + lo, c)]);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+      b[nt] = *reinterpret_cast<const bf16x8*>(&sb[swz32(wn * NT * 32 + nt * 32 + lo, c)]);
+  };
+
+  auto mma = [&](f32x16 (&acc)[4][NT], const bf16x8* a, const bf16x8* b) __attribute__((always_inline)) {
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+        acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mt], b[nt], acc[mt][nt], 0, 0, 0);
+  };
+
+  // Stage q lives in LDS buffer q % 4.  At the barrier of step q every wave
+  // has read all of stage q (both K slices are in registers) and has seen its
+  // own loads of stage q+1 land; after it, stage q+4 is requested into
+  // stage q's buffer.  The inline barrier carries no memory fence, so the
+  // younger stages stay in flight across it.
+  bf16x8 a0[4], b0[NT], a1[4], b1[NT];
+  issue(0);
+  issue(1);
+  issue(2);
+  XC_WAIT_VM_LGKM0(2 * T::LOADS);
+  asm volatile("s_barrier" ::: "memory");
+  issue(3);
+  frags(0, 0, a0, b0);
+  // one step: stage q (in slot B = q mod 4) is multiplied, stage q+4 requested
+  // The scheduling barriers pin the order.  The LDS reads of the next K slice
+  // are issued between the two halves of the current slice's MFMAs, so they
+  // are complete (the compiler waits for all LDS reads before the next
+  // MFMA block) before their MFMAs start; the MFMAs of slice 0 stay ahead of
+  // the workgroup barrier so that they run while the waves meet.
+  auto mma_half = [&](f32x16 (&acc)[4][NT], const bf16x8* a, const bf16x8* b, int h) __attribute__((always_inline)) {
+#pragma unroll
+    for (int mt = 2 * h; mt < 2 * h + 2; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+        acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mt], b[nt], acc[mt][nt], 0, 0, 0);
+  };
+  auto step = [&](f32x16 (&acc)[4][NT], int B) __attribute__((always_inline)) {
+    mma_half(acc, a0, b0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    frags(B, 1, a1, b1);
+    __builtin_amdgcn_sched_barrier(0);
+    mma_half(acc, a0, b0, 1);
+    __builtin_amdgcn_sched_barrier(0);
+    XC_WAIT_VM_LGKM0(2 * T::LOADS);
+    asm volatile("s_barrier" ::: "memory");
+    issue(B);
+    __builtin_amdgcn_sched_barrier(0);
+    mma_half(acc, a1, b1, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    frags((B + 1) & 3, 0, a0, b0);
+    __builtin_amdgcn_sched_barrier(0);
+    mma_half(acc, a1, b1, 1);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // K is a multiple of 128, so every tile starts at slot 0
+  for (int ti = 0; ti < n_my; ++ti) {
+    f32x16 acc[4][NT];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < NT; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    // Unrolled 16 steps deep where K allows: the compiler's own LDS-DMA
+    // bookkeeping drains all requests once per loop iteration.
+    int kt = 0;
+    for (; kt + 16 <= KT; kt += 16) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        step(acc, 0);
+        step(acc, 1);
+        step(acc, 2);
+        step(acc, 3);
+      }
+    }
+    for (; kt < KT; kt += 4) {
+      step(acc, 0);
+      step(acc, 1);
+      step(acc, 2);
+      step(acc, 3);
+    }
+    // ---- epilogue of local tile ti ----
+    int tm, tn;
+    grouped_tile(slot + ti * G, n_tm, n_tn, tm, tn);
+    const int m0 = tm * PBM, n0 = tn * T::BN;
+    // The per-lane row base is made opaque here so that the compiler derives
+    // the epilogue's addresses at the epilogue instead of keeping them live
+    // across the main loop.
+    int rb = wm * 128 + hi * 4;
+    asm volatile("" : "+v"(rb));
+    // accumulator element (mt, nt, g*4 + r): tile row wm*128 + mt*32 + g*8 + hi*4 + r,
+    // tile column wn*32*NT + nt*32 + lo
+    static_assert(MODE != EPI_QKV, "the fused QKV projection runs on the two-workgroup kernel");
+    persistent_epilogue<MODE, NT>(e, acc, m0 + rb, n0 + wn * NT * 32 + lo, M);
+  }
+  // no LDS request may still be landing when the workgroup retires
+  XC_WAIT_VM_LGKM0(0);
+}
+#undef XC_WAIT_VM_LGKM0
+
 template <int MODE>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__ A, const float* __restrict__ W,
                                                        int M, int N, int K, EpiArgs e, const int* __restrict__ flag) {
@@ -344,17 +624,22 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
     }
 }
 
+int cu_count() {
+  static int cus = 0;
+  if (cus == 0) {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cus = n;
+  }
+  return cus;
+}
+
 // Rows per M-tile for an M x N product: the tile height (64*MT) whose tile
 // count best fills whole rounds of resident workgroups (2 per CU).
 int pick_mt(int M, int N) {
-  static int slots = 0;
-  if (slots == 0) {
-    int dev = 0, cus = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-      cus = 256;
-    slots = 2 * cus;
-  }
+  const int slots = 2 * cu_count();
   int best = 4;
   double best_cost = 1e300;
   for (int mt = 4; mt >= 2; --mt) {
@@ -369,6 +654,18 @@ int pick_mt(int M, int N) {
   return best;
 }
 
+// Whether the persistent kernel (256 x 192 tiles) takes an M x N x K product.
+bool use_persistent(int N, int K) { return N % PTile<3>::BN == 0 && K % 128 == 0; }
+
+template <int MODE, int NT>
+void launch_persistent(const void* A, const void* W, int M, int N, int K, const EpiArgs& e, const int* flag,
+                       hipStream_t st) {
+  const int tiles = ((M + PBM - 1) / PBM) * (N / PTile<NT>::BN);
+  int grid = tiles < cu_count() ? tiles : cu_count();
+  if (grid >= kXcd) grid = grid / kXcd * kXcd;
+  gemm_bf16_persistent<MODE, NT><<<grid, 256, 0, st>>>((const bf16*)A, (const bf16*)W, M, N, K, e, flag);
+}
+
 template <int MODE, int MT>
 void launch_bf16(const void* A, const void* W, int M, int N, int K, const EpiArgs& e, const int* flag, hipStream_t st) {
   typedef GemmTile<MT, 2> T;
@@ -381,6 +678,12 @@ template <int MODE>
 void launch_mode(int dtype, const void* A, const void* W, int M, int N, int K, const EpiArgs& e, const int* flag,
                  hipStream_t st) {
   if (dtype == 1) {
+    if constexpr (MODE != EPI_QKV) {
+      if (use_persistent(N, K)) {
+        launch_persistent<MODE, 3>(A, W, M, N, K, e, flag, st);
+        return;
+      }
+    }
     switch (pick_mt(M, N)) {
       case 4: launch_bf16<MODE, 4>(A, W, M, N, K, e, flag, st); break;
       case 3: launch_bf16<MODE, 3>(A, W, M, N, K, e, flag, st); break;

@@ -228,3 +228,20 @@ def test_bf16_three_view_groups():
         ls.run(4, tol_rel_l2=TOLBF)
     finally:
         ls.close()
+
+
+def test_bf16_persistent_gemm_widths():
+    """Widths that are multiples of 192 (hidden 384, MLP 768) take the
+    persistent 256 x 192 projection kernel; L = 300 leaves a ragged last row
+    tile."""
+    w = synth.Workload(
+        "bf16-h384-L300",
+        synth.ModelShape(2, 384, 3, 128, 768, 256, 16, synth.BF16, 4, 2, (synth.ViewGroup(2, 3, 5, 10),)),
+        synth.GateParams(),
+        synth.StreamParams(4, 0.999, 0.02),
+    )
+    ls = _ls(w)
+    try:
+        ls.run(4, tol_rel_l2=TOLBF)
+    finally:
+        ls.close()
