@@ -482,7 +482,7 @@ void build_tables(xc_handle* h) {
   t.n_srows = h->n_srows;
   t.srows = d_rows;
   h->fp_partial = dalloc_t<float>(h, (size_t)t.n_chunks * h->C);
-  h->n_wg = fp_compare_groups_of_wg(h->C);
+  h->n_wg = fp_compare_groups_of_wg(h->C, h->n_srows, h->n_cams);
   h->fp_records = dalloc_t<double>(h, (size_t)h->n_wg * kMaxGroups * kFpRecord);
 }
 

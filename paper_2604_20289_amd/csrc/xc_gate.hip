@@ -2,12 +2,12 @@
 //
 //   fp_colsum   : one read of the block input x; partial column sums over
 //                 16-row chunks that never straddle a camera (HBM-bound).
-//   fp_compare  : per 32-column slice: finishes each camera's token mean
-//                 (global channel), gathers the spatial fingerprint rows,
-//                 accumulates the per-group partial terms of Eq. 5-6 against
-//                 the previous generation's fingerprint and overwrites it with
-//                 the current one (the fingerprint cache is refreshed at every
-//                 evaluation, computed or skipped).
+//   fp_compare  : per 32-column slice, one workgroup for the spatial
+//                 fingerprint rows and one per camera for its token mean
+//                 (global channel); accumulates the per-group partial terms of
+//                 Eq. 5-6 against the previous generation's fingerprint and
+//                 overwrites it with the current one (the fingerprint cache is
+//                 refreshed at every evaluation, computed or skipped).
 //   gate_decide : one workgroup; reduces the partial terms in a fixed order
 //                 (deterministic), forms s = min-cosine and d = max-deviation,
 //                 applies the adaptive threshold (Eq. 8-9), the skip rule
@@ -62,46 +62,111 @@ __device__ __forceinline__ double block_reduce(double v, double* s_red, bool is_
   return r;
 }
 
+// Grid (column slices of 32, spatial row chunks + cameras).  Row y < n_sp
+// handles spatial fingerprint rows [16 y, 16 y + 16) (two per lane); row
+// y = n_sp + v finishes camera v's token mean from its partial column sums:
+// the 8 lanes of a column each sum every 8th chunk (loads issued 4 at a
+// time), and the 8 lane sums are combined in lane order through LDS.  Every
+// workgroup writes one record per group (zeros for terms it does not own); the
+// decision kernel sums the records in a fixed order, so the result is
+// deterministic.
+constexpr int kSpRows = 2 * (256 / kFpCompareCols);  // spatial rows per workgroup
+
 __global__ __launch_bounds__(256) void fp_compare_kernel(const float* __restrict__ x, int C, FpTables t,
                                                          const float* __restrict__ partial,
                                                          float* __restrict__ fp_prev, double* __restrict__ records) {
   __shared__ double s_red[4];
+  __shared__ double s_cam[kFpCompareCols][256 / kFpCompareCols + 1];
   const int cl = threadIdx.x % kFpCompareCols;
   const int rl = threadIdx.x / kFpCompareCols;
   constexpr int kRowLanes = 256 / kFpCompareCols;
   const int c = blockIdx.x * kFpCompareCols + cl;
   const bool col_ok = c < C;
-  for (int g = 0; g < t.n_groups; ++g) {
-    double acc[kRec] = {0, 0, 0, 0, 0, 0, 0, 0};
+  const int wg = blockIdx.y * gridDim.x + blockIdx.x;
+  const int n_sp = (t.n_srows + kSpRows - 1) / kSpRows;
+  if ((int)blockIdx.y < n_sp) {
+    const int i0 = blockIdx.y * kSpRows;
+    const int i1 = min(i0 + kSpRows, t.n_srows);
+    // this lane's two rows: loads first, then the terms
+    const int ia = i0 + rl, ib = i0 + kRowLanes + rl;
+    float cur[2] = {0.f, 0.f}, prev[2] = {0.f, 0.f};
     if (col_ok) {
-      for (int i = t.grp_srow_begin[g] + rl; i < t.grp_srow_begin[g + 1]; i += kRowLanes) {
-        double cur = (double)x[(long long)t.srows[i] * C + c];
-        float* pp = fp_prev + (long long)i * C + c;
-        double prev = (double)*pp;
-        acc[0] += cur * prev;
-        acc[1] += cur * cur;
-        acc[2] += prev * prev;
-        acc[3] = fmax(acc[3], fabs(cur - prev));
-        acc[4] += fabs(prev);
-        *pp = (float)cur;
+      if (ia < i1) {
+        cur[0] = x[(long long)t.srows[ia] * C + c];
+        prev[0] = fp_prev[(long long)ia * C + c];
       }
-      for (int v = t.grp_cam_begin[g] + rl; v < t.grp_cam_begin[g + 1]; v += kRowLanes) {
-        double s = 0.0;
-        for (int k = t.cam_chunk_begin[v]; k < t.cam_chunk_begin[v + 1]; ++k) s += (double)partial[(long long)k * C + c];
-        float mean = (float)(s / (double)t.cam_tokens[v]);
-        double cur = (double)mean;
-        float* pp = fp_prev + (long long)(t.n_srows + v) * C + c;
-        double prev = (double)*pp;
-        acc[5] += cur * prev;
-        acc[6] += cur * cur;
-        acc[7] += prev * prev;
-        *pp = mean;
+      if (ib < i1) {
+        cur[1] = x[(long long)t.srows[ib] * C + c];
+        prev[1] = fp_prev[(long long)ib * C + c];
+      }
+      if (ia < i1) fp_prev[(long long)ia * C + c] = cur[0];
+      if (ib < i1) fp_prev[(long long)ib * C + c] = cur[1];
+    }
+    for (int g = 0; g < t.n_groups; ++g) {
+      double* rec = records + ((long long)wg * kMaxGroups + g) * kRec;
+      const int gb = t.grp_srow_begin[g], ge = t.grp_srow_begin[g + 1];
+      if (ge <= i0 || gb >= i1) {  // no row of this chunk in group g
+        if (threadIdx.x < kRec) rec[threadIdx.x] = 0.0;
+        continue;
+      }
+      double acc[5] = {0, 0, 0, 0, 0};
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int i = u == 0 ? ia : ib;
+        if (col_ok && i < i1 && i >= gb && i < ge) {
+          const double cu = (double)cur[u], pr = (double)prev[u];
+          acc[0] += cu * pr;
+          acc[1] += cu * cu;
+          acc[2] += pr * pr;
+          acc[3] = fmax(acc[3], fabs(cu - pr));
+          acc[4] += fabs(pr);
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < kRec; ++k) {
+        double r = k < 5 ? block_reduce(acc[k], s_red, k == 3) : 0.0;
+        if (threadIdx.x == 0) rec[k] = r;
       }
     }
-    double* rec = records + ((long long)blockIdx.x * kMaxGroups + g) * kRec;
+    return;
+  }
+  const int v = blockIdx.y - n_sp;
+  int gv = 0;
+  while (gv + 1 < t.n_groups && t.grp_cam_begin[gv + 1] <= v) ++gv;
+  double s = 0.0;
+  if (col_ok) {
+    const int k0 = t.cam_chunk_begin[v], k1 = t.cam_chunk_begin[v + 1];
+    int k = k0 + rl;
+    for (; k + 3 * kRowLanes < k1; k += 4 * kRowLanes) {
+      float p[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) p[u] = partial[(long long)(k + u * kRowLanes) * C + c];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) s += (double)p[u];
+    }
+    for (; k < k1; k += kRowLanes) s += (double)partial[(long long)k * C + c];
+  }
+  s_cam[cl][rl] = s;
+  __syncthreads();
+  double acc[3] = {0, 0, 0};
+  if (rl == 0 && col_ok) {
+    double tot = 0.0;
+#pragma unroll
+    for (int r = 0; r < kRowLanes; ++r) tot += s_cam[cl][r];
+    const float mean = (float)(tot / (double)t.cam_tokens[v]);
+    const double cur = (double)mean;
+    float* pp = fp_prev + (long long)(t.n_srows + v) * C + c;
+    const double prev = (double)*pp;
+    acc[0] = cur * prev;
+    acc[1] = cur * cur;
+    acc[2] = prev * prev;
+    *pp = mean;
+  }
+  for (int g = 0; g < t.n_groups; ++g) {
+    double* rec = records + ((long long)wg * kMaxGroups + g) * kRec;
 #pragma unroll
     for (int k = 0; k < kRec; ++k) {
-      double r = block_reduce(acc[k], s_red, k == 3);
+      double r = (g == gv && k >= 5) ? block_reduce(acc[k - 5], s_red, false) : 0.0;
       if (threadIdx.x == 0) rec[k] = r;
     }
   }
@@ -112,9 +177,10 @@ __device__ __forceinline__ double cos_from(double dot, double nn, double pp) {
   return dot / fmax(den, 1e-12);
 }
 
-// One wave.  evaluate == 0: the block is computed without a test (warmup,
-// forced pass, step-0 force, first visit): clear the flag and the staleness.
-__global__ void gate_decide_kernel(const double* __restrict__ records, int n_wg, GateArgs ga, GateState gs,
+// One workgroup of 256 threads.  evaluate == 0: the block is computed without
+// a test (warmup, forced pass, step-0 force, first visit): clear the flag and
+// the staleness.
+__global__ __launch_bounds__(256) void gate_decide_kernel(const double* __restrict__ records, int n_wg, GateArgs ga, GateState gs,
                                    int sb, int b, int evaluate) {
   const int lane = threadIdx.x;
   if (!evaluate) {
@@ -124,23 +190,32 @@ __global__ void gate_decide_kernel(const double* __restrict__ records, int n_wg,
     }
     return;
   }
+  __shared__ double s_red[4];
   double s_min = 1e300, d_max = -1e300;
   for (int g = 0; g < ga.n_groups; ++g) {
-    double tot[kRec];
-    for (int k = 0; k < kRec; ++k) {
-      // lanes stride the workgroup records; a fixed-shape tree keeps the sum deterministic
-      double v = 0.0;
-      for (int w = lane; w < n_wg; w += 64) {
-        double r = records[((long long)w * kMaxGroups + g) * kRec + k];
-        v = (k == 3) ? fmax(v, r) : v + r;
-      }
+    // threads stride the workgroup records (one 64-byte record per load
+    // batch, two batches in flight); fixed-shape reductions keep the sums
+    // deterministic
+    double tot[kRec] = {0, 0, 0, 0, 0, 0, 0, 0};
+    auto add = [&](int w) __attribute__((always_inline)) {
+      const double2* r2 = reinterpret_cast<const double2*>(records + ((long long)w * kMaxGroups + g) * kRec);
+      double2 d[kRec / 2];
 #pragma unroll
-      for (int off = 32; off > 0; off >>= 1) {
-        double o = __shfl_xor(v, off, 64);
-        v = (k == 3) ? fmax(v, o) : v + o;
+      for (int k = 0; k < kRec / 2; ++k) d[k] = r2[k];
+#pragma unroll
+      for (int k = 0; k < kRec / 2; ++k) {
+        tot[2 * k] = (2 * k == 3) ? fmax(tot[2 * k], d[k].x) : tot[2 * k] + d[k].x;
+        tot[2 * k + 1] = (2 * k + 1 == 3) ? fmax(tot[2 * k + 1], d[k].y) : tot[2 * k + 1] + d[k].y;
       }
-      tot[k] = v;
+    };
+    int w = threadIdx.x;
+    for (; w + 256 < n_wg; w += 512) {
+      add(w);
+      add(w + 256);
     }
+    if (w < n_wg) add(w);
+#pragma unroll
+    for (int k = 0; k < kRec; ++k) tot[k] = block_reduce(tot[k], s_red, k == 3);
     double cs = cos_from(tot[0], tot[1], tot[2]);
     double cg = cos_from(tot[5], tot[6], tot[7]);
     double mean_prev = tot[4] / (double)ga.spatial_count[g];
@@ -190,17 +265,20 @@ void launch_fp_colsum(const float* x, int C, const FpTables& t, float* partial, 
   fp_colsum_kernel<<<t.n_chunks, threads, 0, st>>>(x, C, t.chunks, partial);
 }
 
-int fp_compare_groups_of_wg(int C) { return (C + kFpCompareCols - 1) / kFpCompareCols; }
+int fp_compare_groups_of_wg(int C, int n_srows, int n_cams) {
+  return (C + kFpCompareCols - 1) / kFpCompareCols * ((n_srows + kSpRows - 1) / kSpRows + n_cams);
+}
 
 void launch_fp_compare(const float* x, int C, const FpTables& t, const float* partial, float* fp_prev,
                        double* records, hipStream_t st) {
-  fp_compare_kernel<<<fp_compare_groups_of_wg(C), 256, 0, st>>>(x, C, t, partial, fp_prev, records);
+  dim3 grid((C + kFpCompareCols - 1) / kFpCompareCols, (t.n_srows + kSpRows - 1) / kSpRows + t.n_cams);
+  fp_compare_kernel<<<grid, 256, 0, st>>>(x, C, t, partial, fp_prev, records);
 }
 
 void launch_gate_decide(const double* records, int n_wg, const GateArgs& ga, const GateState& gs, int sb, int b,
                         int n_blocks, int evaluate, hipStream_t st) {
   (void)n_blocks;
-  gate_decide_kernel<<<1, 64, 0, st>>>(records, n_wg, ga, gs, sb, b, evaluate);
+  gate_decide_kernel<<<1, 256, 0, st>>>(records, n_wg, ga, gs, sb, b, evaluate);
 }
 
 }  // namespace xc

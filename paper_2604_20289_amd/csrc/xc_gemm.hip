@@ -26,9 +26,15 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
+// tanh-approximated GELU, 0.5 v (1 + tanh(u)) with u = sqrt(2/pi) (v + 0.044715 v^3),
+// evaluated through the identity 0.5 (1 + tanh(u)) = 1 / (1 + e^(-2u)):
+// v / (1 + 2^z), z = -2 log2(e) u, on the hardware exp2 and reciprocal.  For
+// v -> -inf, 2^z -> inf and the result -> -0; no branch, no NaN for finite v.
 __device__ __forceinline__ float gelu_tanh(float v) {
-  const float k0 = 0.7978845608028654f;  // sqrt(2 / pi)
-  return 0.5f * v * (1.0f + tanhf(k0 * (v + 0.044715f * v * v * v)));
+  constexpr float c1 = -2.0f * 0.7978845608028654f * 1.4426950408889634f;  // -2 sqrt(2/pi) log2(e)
+  constexpr float c3 = c1 * 0.044715f;
+  const float z = v * fmaf(c3, v * v, c1);
+  return v * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(z));
 }
 
 template <typename T>

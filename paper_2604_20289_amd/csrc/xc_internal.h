@@ -112,7 +112,8 @@ void launch_pass_begin(const GateState& gs, int n_blocks, hipStream_t st);
 void launch_fp_colsum(const float* x, int C, const FpTables& t, float* partial, hipStream_t st);
 void launch_fp_compare(const float* x, int C, const FpTables& t, const float* partial, float* fp_prev,
                        double* records, hipStream_t st);
-int fp_compare_groups_of_wg(int C);
+// Partial records written by the comparison kernel (per group each).
+int fp_compare_groups_of_wg(int C, int n_srows, int n_cams);
 void launch_gate_decide(const double* records, int n_wg, const GateArgs& ga, const GateState& gs, int S_idx,
                         int b, int n_blocks, int evaluate, hipStream_t st);
 void launch_fill_f32(float* p, float v, long long n, hipStream_t st);
