@@ -46,20 +46,31 @@ __global__ __launch_bounds__(1024) void fp_colsum_kernel(const float* __restrict
   }
 }
 
-__device__ __forceinline__ double block_reduce(double v, double* s_red, bool is_max) {
-  // 256 threads: wave reduction, then across the 4 waves through LDS.
+// Block reduction of NF fields at once (256 threads): the per-field
+// shuffle chains are independent, so their latencies overlap; one LDS
+// exchange across the 4 waves.  Field `max_field` takes the maximum, the
+// others the sum; fixed order throughout.
+template <int NF>
+__device__ __forceinline__ void block_reduce_n(double (&v)[NF], double* s_red, int max_field) {
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    double o = __shfl_xor(v, off, 64);
-    v = is_max ? fmax(v, o) : v + o;
-  }
+  for (int off = 32; off > 0; off >>= 1)
+#pragma unroll
+    for (int f = 0; f < NF; ++f) {
+      const double o = __shfl_xor(v[f], off, 64);
+      v[f] = f == max_field ? fmax(v[f], o) : v[f] + o;
+    }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   __syncthreads();
-  if (lane == 0) s_red[wave] = v;
+  if (lane == 0)
+#pragma unroll
+    for (int f = 0; f < NF; ++f) s_red[wave * NF + f] = v[f];
   __syncthreads();
-  double r = s_red[0];
-  for (int w = 1; w < 4; ++w) r = is_max ? fmax(r, s_red[w]) : r + s_red[w];
-  return r;
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    double r = s_red[f];
+    for (int w = 1; w < 4; ++w) r = f == max_field ? fmax(r, s_red[w * NF + f]) : r + s_red[w * NF + f];
+    v[f] = r;
+  }
 }
 
 // Grid (column slices of 32, spatial row chunks + cameras).  Row y < n_sp
@@ -75,7 +86,7 @@ constexpr int kSpRows = 2 * (256 / kFpCompareCols);  // spatial rows per workgro
 __global__ __launch_bounds__(256) void fp_compare_kernel(const float* __restrict__ x, int C, FpTables t,
                                                          const float* __restrict__ partial,
                                                          float* __restrict__ fp_prev, double* __restrict__ records) {
-  __shared__ double s_red[4];
+  __shared__ double s_red[4 * 5];
   __shared__ double s_cam[kFpCompareCols][256 / kFpCompareCols + 1];
   const int cl = threadIdx.x % kFpCompareCols;
   const int rl = threadIdx.x / kFpCompareCols;
@@ -122,11 +133,10 @@ __global__ __launch_bounds__(256) void fp_compare_kernel(const float* __restrict
           acc[4] += fabs(pr);
         }
       }
+      block_reduce_n<5>(acc, s_red, 3);
+      if (threadIdx.x == 0)
 #pragma unroll
-      for (int k = 0; k < kRec; ++k) {
-        double r = k < 5 ? block_reduce(acc[k], s_red, k == 3) : 0.0;
-        if (threadIdx.x == 0) rec[k] = r;
-      }
+        for (int k = 0; k < kRec; ++k) rec[k] = k < 5 ? acc[k < 5 ? k : 0] : 0.0;
     }
     return;
   }
@@ -162,13 +172,12 @@ __global__ __launch_bounds__(256) void fp_compare_kernel(const float* __restrict
     acc[2] = prev * prev;
     *pp = mean;
   }
+  block_reduce_n<3>(acc, s_red, -1);
   for (int g = 0; g < t.n_groups; ++g) {
     double* rec = records + ((long long)wg * kMaxGroups + g) * kRec;
+    if (threadIdx.x == 0)
 #pragma unroll
-    for (int k = 0; k < kRec; ++k) {
-      double r = (g == gv && k >= 5) ? block_reduce(acc[k - 5], s_red, false) : 0.0;
-      if (threadIdx.x == 0) rec[k] = r;
-    }
+      for (int k = 0; k < kRec; ++k) rec[k] = (g == gv && k >= 5) ? acc[k >= 5 ? k - 5 : 0] : 0.0;
   }
 }
 
@@ -190,7 +199,7 @@ __global__ __launch_bounds__(256) void gate_decide_kernel(const double* __restri
     }
     return;
   }
-  __shared__ double s_red[4];
+  __shared__ double s_red[4 * kRec];
   double s_min = 1e300, d_max = -1e300;
   for (int g = 0; g < ga.n_groups; ++g) {
     // threads stride the workgroup records (one 64-byte record per load
@@ -214,8 +223,7 @@ __global__ __launch_bounds__(256) void gate_decide_kernel(const double* __restri
       add(w + 256);
     }
     if (w < n_wg) add(w);
-#pragma unroll
-    for (int k = 0; k < kRec; ++k) tot[k] = block_reduce(tot[k], s_red, k == 3);
+    block_reduce_n<kRec>(tot, s_red, 3);
     double cs = cos_from(tot[0], tot[1], tot[2]);
     double cg = cos_from(tot[5], tot[6], tot[7]);
     double mean_prev = tot[4] / (double)ga.spatial_count[g];
