@@ -77,13 +77,14 @@ def attention_flops(m, n_keys):
     return 4.0 * m.tokens * n_keys * m.n_heads * m.head_dim
 
 
-def run_stream(xc, m, eps_dev, actions, n_warm, n_timed, torch, profile=False, on_profile_start=None):
-    """Drive n_warm + n_timed chunks; returns per-chunk ms of the timed ones."""
+def run_stream(xc, m, eps_dev, actions, n_warm, n_timed, torch, profile=False):
+    """Drive n_warm + n_timed chunks; returns, per timed chunk, (chunk ms, ms of
+    the S denoising passes, ms of the KV-update pass)."""
     L, C = m.tokens, m.hidden
     taus = synth.timesteps(m)
     x = torch.empty((L, C), dtype=torch.float32, device="cuda")
     y = torch.empty_like(x)
-    ms = []
+    ev = []
     for n in range(n_warm + n_timed):
         eps = eps_dev[n]
         timed = n >= n_warm
@@ -92,23 +93,24 @@ def run_stream(xc, m, eps_dev, actions, n_warm, n_timed, torch, profile=False, o
             if profile:
                 xc.profile(True)
         if timed:
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
-            e0.record()
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            e[0].record()
         x.copy_(eps)
         for t in range(m.n_steps):
             xc.forward_chunk(t, taus[t], actions[n], x, y)
             if t + 1 < m.n_steps:
                 sg = synth.sampler_sigma(m, t + 1)
                 xc.axpby(1.0 - sg, y, sg, eps, x, L * C)
+        if timed:
+            e[1].record()
         xc.kv_update(synth.KV_UPDATE_TIMESTEP, actions[n], y, None)
         if timed:
-            e1.record()
-            ms.append((e0, e1))
+            e[2].record()
+            ev.append(e)
     torch.cuda.synchronize()
     if profile:
         xc.profile(False)
-    return [a.elapsed_time(b) for a, b in ms]
+    return [(e[0].elapsed_time(e[2]), e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2])) for e in ev]
 
 
 def kernel_table(xc, xcp):
@@ -154,6 +156,7 @@ def main():
     ap.add_argument("--tau-floor", type=float, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gate-off", action="store_true")
+    ap.add_argument("--no-alt-tau", action="store_true", help="skip the extra gate-on run at tau_floor 0.95")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="copy a buffer of this many MiB once (calibrates rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     args = ap.parse_args()
@@ -194,7 +197,8 @@ def main():
 
     # 1. gate on
     xc = xcp.XCache(m, w.gate, weights, stream)
-    on_ms = run_stream(xc, m, eps_dev, actions, args.warmup, args.steps, torch)
+    on_split = run_stream(xc, m, eps_dev, actions, args.warmup, args.steps, torch)
+    on_ms = [v[0] for v in on_split]
     st = xc.stats()
     # 3. gate kernels (same handle, two more chunks continue the stream state)
     xc.reset()
@@ -205,11 +209,24 @@ def main():
     log(f"gate on: mean {statistics.mean(on_ms):.2f} ms/chunk, skips {st['skips']} / "
         f"{st['evals_post_warmup']}")
 
+    # 1b. the same stream at the other tau_floor the paper states (0.95 vs Table 1's 0.97)
+    alt = None
+    if args.tau_floor is None and not args.no_alt_tau:
+        wa = synth.with_gate(w, tau_floor=0.95)
+        xc = xcp.XCache(m, wa.gate, weights, stream)
+        alt_ms = [v[0] for v in run_stream(xc, m, eps_dev, actions, args.warmup, args.steps, torch)]
+        sa = xc.stats()
+        xc.close()
+        alt = {"tau_floor": 0.95, "value": round(statistics.mean(alt_ms), 3),
+               "chunk_ms_median": round(statistics.median(alt_ms), 3),
+               "skip_rate": round(sa["skips"] / max(1, sa["evals_post_warmup"]), 4)}
+        log(f"tau_floor 0.95: mean {alt['value']:.2f} ms/chunk, skip rate {alt['skip_rate']:.3f}")
+
     # 2. gate off
     off_ms, kt = None, {}
     if not args.no_gate_off:
         xc = xcp.XCache(m, synth.with_gate(w, enabled=0).gate, weights, stream)
-        off_ms = run_stream(xc, m, eps_dev, actions, args.warmup, args.steps, torch, profile=True)
+        off_ms = [v[0] for v in run_stream(xc, m, eps_dev, actions, args.warmup, args.steps, torch, profile=True)]
         kt = kernel_table(xc, xcp)
         xc.close()
         log(f"gate off: mean {statistics.mean(off_ms):.2f} ms/chunk")
@@ -241,10 +258,19 @@ def main():
                    else f"Table 1 with tau_floor={args.tau_floor}", "steady_state_window": steady},
         "chunk_ms_median": round(statistics.median(on_ms), 3),
         "chunk_ms": [round(v, 2) for v in on_ms],
+        "passes_ms_mean": round(statistics.mean(v[1] for v in on_split), 3),
+        "kv_update_ms_mean": round(statistics.mean(v[2] for v in on_split), 3),
         "skip_rate": round(skip_rate, 4),
         "skips": st["skips"],
         "block_evals_post_warmup": st["evals_post_warmup"],
+        # per (denoising step t, block b): skips over the whole stream, and the
+        # gate's running cosine average s-bar after the last chunk
+        "skip_counts_tb": np.asarray(st["skip_counts"]).reshape(S, B).astype(int).tolist(),
+        "ema_cos_tb": [[None if not np.isfinite(v) else round(float(v), 5) for v in row]
+                       for row in np.asarray(st["ema"]).reshape(S, B)],
     }
+    if alt:
+        res["alt_tau_floor"] = alt
     if off_ms:
         off_mean = statistics.mean(off_ms)
         chunk_flops = fl_block * B * (S + 1)
