@@ -77,9 +77,12 @@ def attention_flops(m, n_keys):
     return 4.0 * m.tokens * n_keys * m.n_heads * m.head_dim
 
 
-def run_stream(xc, m, eps_dev, actions, n_warm, n_timed, torch, profile=False):
+def run_stream(xc, m, eps_dev, actions, n_warm, n_timed, torch, profile=False, force_every=0, per_chunk=None):
     """Drive n_warm + n_timed chunks; returns, per timed chunk, (chunk ms, ms of
-    the S denoising passes, ms of the KV-update pass)."""
+    the S denoising passes, ms of the KV-update pass).  force_every = P > 0
+    computes every block of the denoising passes of chunks n with n % P == 0
+    (the paper's periodic whole-generation refresh); per_chunk, a list, then
+    receives each chunk's skip count (the stream is synchronised per chunk)."""
     L, C = m.tokens, m.hidden
     taus = synth.timesteps(m)
     x = torch.empty((L, C), dtype=torch.float32, device="cuda")
@@ -96,8 +99,9 @@ def run_stream(xc, m, eps_dev, actions, n_warm, n_timed, torch, profile=False):
             e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
             e[0].record()
         x.copy_(eps)
+        fl = xcp_force_full if force_every and n % force_every == 0 else 0
         for t in range(m.n_steps):
-            xc.forward_chunk(t, taus[t], actions[n], x, y)
+            xc.forward_chunk(t, taus[t], actions[n], x, y, fl)
             if t + 1 < m.n_steps:
                 sg = synth.sampler_sigma(m, t + 1)
                 xc.axpby(1.0 - sg, y, sg, eps, x, L * C)
@@ -107,10 +111,15 @@ def run_stream(xc, m, eps_dev, actions, n_warm, n_timed, torch, profile=False):
         if timed:
             e[2].record()
             ev.append(e)
+        if per_chunk is not None:
+            per_chunk.append(xc.stats()["skips"])
     torch.cuda.synchronize()
     if profile:
         xc.profile(False)
     return [(e[0].elapsed_time(e[2]), e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2])) for e in ev]
+
+
+xcp_force_full = 1  # the library's forward flag that computes every block (set from the binding in main)
 
 
 def kernel_table(xc, xcp):
@@ -157,6 +166,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gate-off", action="store_true")
     ap.add_argument("--no-alt-tau", action="store_true", help="skip the extra gate-on run at tau_floor 0.95")
+    ap.add_argument("--force-every", type=int, default=0,
+                    help="also run the gate-on stream with every P-th generation computed in full and report "
+                         "the per-chunk skip fractions (the paper's periodic refresh cadence)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="copy a buffer of this many MiB once (calibrates rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     args = ap.parse_args()
@@ -168,6 +180,8 @@ def main():
 
     import torch
     from paper_2604_20289_amd import xcache as xcp
+    global xcp_force_full
+    xcp_force_full = xcp.XC_FORCE_FULL
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
@@ -222,6 +236,20 @@ def main():
                "skip_rate": round(sa["skips"] / max(1, sa["evals_post_warmup"]), 4)}
         log(f"tau_floor 0.95: mean {alt['value']:.2f} ms/chunk, skip rate {alt['skip_rate']:.3f}")
 
+    # 1c. periodic whole-generation refresh: skip fraction per chunk
+    cadence = None
+    if args.force_every > 0:
+        xc = xcp.XCache(m, w.gate, weights, stream)
+        counts = []
+        cad_ms = [v[0] for v in run_stream(xc, m, eps_dev, actions, 0, n_chunks, torch,
+                                           force_every=args.force_every, per_chunk=counts)]
+        xc.close()
+        per = [c - p for c, p in zip(counts, [0] + counts[:-1])]
+        denom = m.n_blocks * m.n_steps
+        cadence = {"force_every": args.force_every, "chunk_skip_fraction": [round(c / denom, 4) for c in per],
+                   "mean_ms_after_warmup": round(statistics.mean(cad_ms[args.warmup:]), 3)}
+        log(f"force every {args.force_every}: skip fractions {cadence['chunk_skip_fraction']}")
+
     # 2. gate off
     off_ms, kt = None, {}
     if not args.no_gate_off:
@@ -271,6 +299,8 @@ def main():
     }
     if alt:
         res["alt_tau_floor"] = alt
+    if cadence:
+        res["periodic_refresh"] = cadence
     if off_ms:
         off_mean = statistics.mean(off_ms)
         chunk_flops = fl_block * B * (S + 1)

@@ -57,6 +57,10 @@ typedef enum xc_status {
 enum { XC_F32 = 0, XC_BF16 = 1 };
 enum { XC_STEP0_OFF = 0, XC_STEP0_FORCE = 1, XC_STEP0_STRICT = 2 };
 enum { XC_FP_GRID3D = 0, XC_FP_LINSPACE1D = 1 };
+/* When the cached fingerprint of (t, b) is replaced by the current one
+   (Section 2.5 says the fingerprint cache stays refreshed; the paper does not
+   say whether a skipped evaluation refreshes it). */
+enum { XC_FP_REFRESH_EVERY = 0, XC_FP_REFRESH_ON_COMPUTE = 1 };
 /* xc_forward_chunk flags */
 enum { XC_FORCE_FULL = 1u };
 /* per-block decision codes reported by xc_stats for the last denoising pass */
@@ -117,6 +121,8 @@ typedef struct xc_gate_config {
   float tau_strict0;      /* strict step-0 threshold (0.999)                  */
   int32_t kv_protect;     /* must be 1: KV-update passes are never gated      */
   int32_t fp_mode;        /* XC_FP_GRID3D or XC_FP_LINSPACE1D                 */
+  int32_t fp_refresh;     /* XC_FP_REFRESH_EVERY: at every evaluation (0);    */
+                          /* XC_FP_REFRESH_ON_COMPUTE: only when computed     */
 } xc_gate_config;
 
 typedef struct xc_stats_t {

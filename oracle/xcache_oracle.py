@@ -56,6 +56,7 @@ import synth
 FORCE_FULL = 1           # forward flag: compute every block, still refresh caches
 STEP0_OFF, STEP0_FORCE, STEP0_STRICT = 0, 1, 2
 FP_GRID3D, FP_LINSPACE1D = 0, 1
+FP_REFRESH_EVERY, FP_REFRESH_ON_COMPUTE = 0, 1   # when phi_prev takes the current fingerprint
 
 # decision codes reported per block and pass
 DEC_COMPUTE = 0          # gate evaluated, test failed -> computed
@@ -376,7 +377,9 @@ class XCacheOracle:
                     skip = bool(decide(b, info))
                 info["decision"] = DEC_SKIP if skip else DEC_COMPUTE
                 self.gated_evals += 1
-            if gate_b:
+            # Section 2.5 keeps the fingerprint cache refreshed; by default at
+            # every evaluation of (t, b), alternatively only when it computes
+            if gate_b and (g.fp_refresh == FP_REFRESH_EVERY or not skip):
                 self.fp_prev[key] = fp
             if skip:
                 x = x + self.rhat[key]

@@ -57,6 +57,8 @@ struct xc_handle {
   void* w2 = nullptr; float* b2 = nullptr;
   // caches
   void* kc = nullptr; void* vt = nullptr; void* rhat = nullptr; float* fp = nullptr;
+  float* fp_alt = nullptr;  // second fingerprint set of the refresh-on-compute mode
+  int* fp_sel = nullptr;     // [S][B] which of fp / fp_alt holds the cached fingerprint
   // gate state
   float* ema = nullptr; int* stale = nullptr; int* skip_counts = nullptr; int* flags = nullptr;
   int* rec_dec = nullptr; float* rec_s = nullptr; float* rec_d = nullptr; float* rec_tau = nullptr;
@@ -145,6 +147,7 @@ xc_status validate_gate(const xc_gate_config* g, const xc_model_config* m) {
   if (g->max_stale < 0) return XC_ERR_INVALID_ARG;
   if (g->step0_mode < XC_STEP0_OFF || g->step0_mode > XC_STEP0_STRICT) return XC_ERR_INVALID_ARG;
   if (g->fp_mode != XC_FP_GRID3D && g->fp_mode != XC_FP_LINSPACE1D) return XC_ERR_INVALID_ARG;
+  if (g->fp_refresh != XC_FP_REFRESH_EVERY && g->fp_refresh != XC_FP_REFRESH_ON_COMPUTE) return XC_ERR_INVALID_ARG;
   if (g->kv_protect == 0) return XC_ERR_UNSUPPORTED;
   if (g->kv_protect != 1) return XC_ERR_INVALID_ARG;
   (void)m;
@@ -315,6 +318,7 @@ GateState gate_state(xc_handle* h) {
   gs.rec_s = h->rec_s;
   gs.rec_d = h->rec_d;
   gs.rec_tau = h->rec_tau;
+  gs.fp_sel = h->fp_sel;
   return gs;
 }
 
@@ -491,6 +495,8 @@ void reset_state(xc_handle* h) {
   XC_HIP(hipMemsetAsync(h->kc, 0, (size_t)h->B * h->H * h->Lcap * h->D * h->esz, h->st));
   XC_HIP(hipMemsetAsync(h->vt, 0, (size_t)h->B * h->H * h->Lcap * h->D * h->esz, h->st));
   if (h->fp) XC_HIP(hipMemsetAsync(h->fp, 0, SB * h->fp_rows * h->C * sizeof(float), h->st));
+  if (h->fp_alt) XC_HIP(hipMemsetAsync(h->fp_alt, 0, SB * h->fp_rows * h->C * sizeof(float), h->st));
+  if (h->fp_sel) XC_HIP(hipMemsetAsync(h->fp_sel, 0, SB * sizeof(int), h->st));
   launch_fill_f32(h->ema, __builtin_nanf(""), (long long)SB, h->st);
   XC_HIP(hipMemsetAsync(h->stale, 0, SB * sizeof(int), h->st));
   XC_HIP(hipMemsetAsync(h->skip_counts, 0, SB * sizeof(int), h->st));
@@ -607,6 +613,10 @@ void init_device(xc_handle* h, const float* w) {
   XC_HIP(hipMemsetAsync(h->u, 0, (size_t)h->Mpad * Dm * esz, h->st));
   build_tables(h);
   if (h->g.enabled) h->fp = dalloc_t<float>(h, SB * h->fp_rows * C);
+  if (h->g.enabled && h->g.fp_refresh == XC_FP_REFRESH_ON_COMPUTE) {
+    h->fp_alt = dalloc_t<float>(h, SB * h->fp_rows * C);
+    h->fp_sel = dalloc_t<int>(h, SB);
+  }
   reset_state(h);
 }
 
@@ -732,8 +742,9 @@ xc_status xc_forward_chunk(xc_handle* h, int32_t step, float timestep, const flo
         }
         {
           Prof p(h, XC_KERN_GATE_COMPARE);
-          launch_fp_compare(x, h->C, h->tables, h->fp_partial, h->fp + sb * h->fp_rows * h->C, h->fp_records,
-                            h->st);
+          const size_t fo = sb * h->fp_rows * h->C;
+          launch_fp_compare(x, h->C, h->tables, h->fp_partial, h->fp + fo, h->fp_alt ? h->fp_alt + fo : nullptr,
+                            h->fp_sel ? h->fp_sel + sb : nullptr, h->fp_records, h->st);
         }
         const bool evaluate = !forced_all && h->visited[sb];
         {

@@ -84,8 +84,12 @@ __device__ __forceinline__ void block_reduce_n(double (&v)[NF], double* s_red, i
 constexpr int kSpRows = 2 * (256 / kFpCompareCols);  // spatial rows per workgroup
 
 __global__ __launch_bounds__(256) void fp_compare_kernel(const float* __restrict__ x, int C, FpTables t,
-                                                         const float* __restrict__ partial,
-                                                         float* __restrict__ fp_prev, double* __restrict__ records) {
+                                                         const float* __restrict__ partial, float* fp0, float* fp1,
+                                                         const int* __restrict__ sel, double* __restrict__ records) {
+  // cached fingerprint and where the current one goes
+  const bool flip = sel != nullptr && *sel != 0;
+  const float* fp_prev = flip ? fp1 : fp0;
+  float* fp_cur = sel == nullptr ? fp0 : (flip ? fp0 : fp1);
   __shared__ double s_red[4 * 5];
   __shared__ double s_cam[kFpCompareCols][256 / kFpCompareCols + 1];
   const int cl = threadIdx.x % kFpCompareCols;
@@ -110,8 +114,8 @@ __global__ __launch_bounds__(256) void fp_compare_kernel(const float* __restrict
         cur[1] = x[(long long)t.srows[ib] * C + c];
         prev[1] = fp_prev[(long long)ib * C + c];
       }
-      if (ia < i1) fp_prev[(long long)ia * C + c] = cur[0];
-      if (ib < i1) fp_prev[(long long)ib * C + c] = cur[1];
+      if (ia < i1) fp_cur[(long long)ia * C + c] = cur[0];
+      if (ib < i1) fp_cur[(long long)ib * C + c] = cur[1];
     }
     for (int g = 0; g < t.n_groups; ++g) {
       double* rec = records + ((long long)wg * kMaxGroups + g) * kRec;
@@ -165,12 +169,12 @@ __global__ __launch_bounds__(256) void fp_compare_kernel(const float* __restrict
     for (int r = 0; r < kRowLanes; ++r) tot += s_cam[cl][r];
     const float mean = (float)(tot / (double)t.cam_tokens[v]);
     const double cur = (double)mean;
-    float* pp = fp_prev + (long long)(t.n_srows + v) * C + c;
-    const double prev = (double)*pp;
+    const long long ip = (long long)(t.n_srows + v) * C + c;
+    const double prev = (double)fp_prev[ip];
     acc[0] = cur * prev;
     acc[1] = cur * cur;
     acc[2] = prev * prev;
-    *pp = mean;
+    fp_cur[ip] = mean;
   }
   block_reduce_n<3>(acc, s_red, -1);
   for (int g = 0; g < t.n_groups; ++g) {
@@ -196,6 +200,7 @@ __global__ __launch_bounds__(256) void gate_decide_kernel(const double* __restri
     if (lane == 0) {
       gs.flags[b] = 0;
       gs.stale[sb] = 0;
+      if (gs.fp_sel != nullptr) gs.fp_sel[sb] ^= 1;  // computed: the current fingerprint becomes the cached one
     }
     return;
   }
@@ -258,6 +263,7 @@ __global__ __launch_bounds__(256) void gate_decide_kernel(const double* __restri
   const bool skip = (s_min >= tau) && (d_max < (double)ga.tau_dev) && (ga.max_stale == 0 || stale < ga.max_stale);
   gs.flags[b] = skip ? 1 : 0;
   gs.stale[sb] = skip ? stale + 1 : 0;
+  if (gs.fp_sel != nullptr && !skip) gs.fp_sel[sb] ^= 1;
   if (skip) gs.skip_counts[sb] += 1;
   gs.rec_dec[b] = skip ? 1 : 0;
   gs.rec_s[b] = (float)s_min;
@@ -277,10 +283,10 @@ int fp_compare_groups_of_wg(int C, int n_srows, int n_cams) {
   return (C + kFpCompareCols - 1) / kFpCompareCols * ((n_srows + kSpRows - 1) / kSpRows + n_cams);
 }
 
-void launch_fp_compare(const float* x, int C, const FpTables& t, const float* partial, float* fp_prev,
-                       double* records, hipStream_t st) {
+void launch_fp_compare(const float* x, int C, const FpTables& t, const float* partial, float* fp0, float* fp1,
+                       const int* sel, double* records, hipStream_t st) {
   dim3 grid((C + kFpCompareCols - 1) / kFpCompareCols, (t.n_srows + kSpRows - 1) / kSpRows + t.n_cams);
-  fp_compare_kernel<<<grid, 256, 0, st>>>(x, C, t, partial, fp_prev, records);
+  fp_compare_kernel<<<grid, 256, 0, st>>>(x, C, t, partial, fp0, fp1, sel, records);
 }
 
 void launch_gate_decide(const double* records, int n_wg, const GateArgs& ga, const GateState& gs, int sb, int b,

@@ -72,6 +72,8 @@ struct GateState {
   float* rec_s;        // [B]
   float* rec_d;        // [B]
   float* rec_tau;      // [B]
+  int* fp_sel;         // [S][B] refresh-on-compute mode: which fingerprint set holds (t, b)'s
+                       // cached fingerprint, flipped when the block computes; null otherwise
 };
 
 // Fingerprint tables (device).
@@ -110,8 +112,11 @@ void launch_skip_add(int dtype, const float* x, const void* rhat, float* out, lo
 void launch_axpby(float a, const float* x, float b, const float* y, float* out, long long n, hipStream_t st);
 void launch_pass_begin(const GateState& gs, int n_blocks, hipStream_t st);
 void launch_fp_colsum(const float* x, int C, const FpTables& t, float* partial, hipStream_t st);
-void launch_fp_compare(const float* x, int C, const FpTables& t, const float* partial, float* fp_prev,
-                       double* records, hipStream_t st);
+// fp0 / fp1: the (t, b) fingerprint sets; with sel == null the cached
+// fingerprint is fp0 and is overwritten in place, otherwise it is fp[*sel] and
+// the current one goes to the other set.
+void launch_fp_compare(const float* x, int C, const FpTables& t, const float* partial, float* fp0, float* fp1,
+                       const int* sel, double* records, hipStream_t st);
 // Partial records written by the comparison kernel (per group each).
 int fp_compare_groups_of_wg(int C, int n_srows, int n_cams);
 void launch_gate_decide(const double* records, int n_wg, const GateArgs& ga, const GateState& gs, int S_idx,

@@ -22,6 +22,7 @@ XC_OK, XC_ERR_INVALID_ARG, XC_ERR_STATE, XC_ERR_OOM, XC_ERR_HIP, XC_ERR_UNSUPPOR
 XC_F32, XC_BF16 = 0, 1
 XC_STEP0_OFF, XC_STEP0_FORCE, XC_STEP0_STRICT = 0, 1, 2
 XC_FP_GRID3D, XC_FP_LINSPACE1D = 0, 1
+XC_FP_REFRESH_EVERY, XC_FP_REFRESH_ON_COMPUTE = 0, 1
 XC_FORCE_FULL = 1
 XC_DEC_COMPUTE, XC_DEC_SKIP, XC_DEC_FORCED, XC_DEC_NONE = 0, 1, 2, 255
 XC_MAX_GROUPS = 8
@@ -55,7 +56,8 @@ class GateConfigC(ctypes.Structure):
                 ("adaptive", ctypes.c_int32), ("tau_floor", ctypes.c_float), ("margin", ctypes.c_float),
                 ("alpha", ctypes.c_float), ("tau_cos_fixed", ctypes.c_float), ("tau_dev", ctypes.c_float),
                 ("eps", ctypes.c_float), ("max_stale", ctypes.c_int32), ("step0_mode", ctypes.c_int32),
-                ("tau_strict0", ctypes.c_float), ("kv_protect", ctypes.c_int32), ("fp_mode", ctypes.c_int32)]
+                ("tau_strict0", ctypes.c_float), ("kv_protect", ctypes.c_int32), ("fp_mode", ctypes.c_int32),
+                ("fp_refresh", ctypes.c_int32)]
 
 
 class StatsC(ctypes.Structure):

@@ -98,6 +98,7 @@ class GateParams:
     tau_strict0: float = 0.999
     kv_protect: int = 1
     fp_mode: int = 0              # 0 3-D grid, 1 1-D linspace fallback
+    fp_refresh: int = 0           # 0 at every evaluation, 1 only when the block is computed
 
 
 @dataclasses.dataclass(frozen=True)

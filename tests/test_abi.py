@@ -76,6 +76,7 @@ def test_init_rejects_bad_model(change, want):
     (dict(alpha=1.5), xcp.XC_ERR_INVALID_ARG),
     (dict(step0_mode=3), xcp.XC_ERR_INVALID_ARG),
     (dict(fp_mode=2), xcp.XC_ERR_INVALID_ARG),
+    (dict(fp_refresh=2), xcp.XC_ERR_INVALID_ARG),
     (dict(fp_budget=0), xcp.XC_ERR_INVALID_ARG),
     (dict(tau_floor=math.nan), xcp.XC_ERR_INVALID_ARG),
     (dict(eps=-1.0), xcp.XC_ERR_INVALID_ARG),

@@ -51,6 +51,8 @@ CFG0_VARIANTS = {
                                                      max_stale=1), rho=0.999),
     "back-anchor-4blk": synth.with_stream(synth.with_model(
         synth.with_gate(W0, adaptive=1, tau_floor=0.97, tau_dev=2.0, back_anchors=1), n_blocks=4), rho=0.999),
+    "refresh-on-compute": synth.with_stream(synth.with_gate(W0, adaptive=1, tau_floor=0.97, tau_dev=2.0,
+                                                            fp_refresh=xo.FP_REFRESH_ON_COMPUTE), rho=0.999),
     "gate-off": synth.with_gate(W0, enabled=0),
     "window-1": synth.with_stream(synth.with_model(synth.with_gate(W0, adaptive=1, tau_floor=0.9, tau_dev=2.0),
                                                    kv_window=1), rho=0.999),

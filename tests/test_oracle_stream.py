@@ -239,6 +239,42 @@ def test_force_full_flag_computes_and_refreshes():
     assert any(x["decision"] == xo.DEC_SKIP for n, t, r in rec if n == 3 for x in r)
 
 
+def test_fingerprint_refresh_modes():
+    """Every evaluation replaces the cached fingerprint by default; in the
+    refresh-on-compute mode a skipped evaluation leaves the one of the last
+    computed pass (here chunk 0, since every later gated evaluation skips)."""
+    import copy
+    base = synth.with_stream(synth.with_gate(synth.workload(0), adaptive=0, tau_cos_fixed=-1.0, tau_dev=math.inf,
+                                             front_anchors=0), rho=0.9)
+    snaps = {}
+    for mode in (xo.FP_REFRESH_EVERY, xo.FP_REFRESH_ON_COMPUTE):
+        w = synth.with_gate(base, fp_refresh=mode)
+        m = w.model
+        orc = xo.XCacheOracle(m, w.gate, synth.make_weights(m))
+        eps = list(synth.latent_stream(m, w.stream, 0, 3))
+        acts = list(synth.action_stream(m, w.stream, 0, 3))
+        after0, svals = None, []
+        for n in range(3):
+            x = eps[n].astype(np.float64)
+            for t in range(m.n_steps):
+                y = orc.forward_chunk(t, 1000.0 * (1 - t / m.n_steps), acts[n], x)
+                if n > 0:
+                    assert all(r["decision"] == xo.DEC_SKIP for r in orc.last)
+                    svals.append(orc.last[0]["s"])
+                x = y
+            orc.kv_update(0.0, acts[n], y)
+            if n == 0:
+                after0 = copy.deepcopy(orc.fp_prev)
+        same = all(np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+                   for k in after0 for a, b in zip(after0[k], orc.fp_prev[k]))
+        assert same == (mode == xo.FP_REFRESH_ON_COMPUTE)
+        snaps[mode] = svals
+    # chunk 1 compares with chunk 0 in both modes; chunk 2 with chunk 1 (every) or chunk 0 (on compute)
+    S = base.model.n_steps
+    assert snaps[0][:S] == snaps[1][:S]
+    assert snaps[0][S:] != snaps[1][S:]
+
+
 def test_fifo_eviction_keeps_last_window():
     w = synth.with_model(synth.workload(0), kv_window=3)
     m = w.model
