@@ -4,8 +4,10 @@
 // the per-head cache, so the kernel sees one key range.
 //
 // bf16 path (flash-style, one pass over the keys with an online softmax):
-//   * workgroup = 4 waves = 128 queries of one head; each wave owns 32 queries
-//     whose Q fragments stay in registers for the whole key loop;
+//   * workgroup = 8 waves = 256 queries of one head (one workgroup per CU,
+//     two waves per SIMD); each wave owns 32 queries whose Q fragments stay in
+//     registers for the whole key loop, and the 8 waves share every staged
+//     K / V^T tile;
 //   * per 64-key tile, S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (keys on the
 //     MFMA rows, queries on the columns), so each lane holds 32 scores of ONE
 //     query: the running max/sum and the output rescale are lane-local except
@@ -16,7 +18,8 @@
 //     are exactly the 8 consecutive keys the P operand needs (no shuffles);
 //   * K and V^T tiles are double-buffered in LDS (rows padded by 16 bytes);
 //     scores are scaled into the log2 domain by one FMA and exponentiated
-//     with exp2; accumulation is float.
+//     with exp2; the softmax denominator sums the bf16 probabilities that the
+//     P.V product consumes (two per dot2 instruction); accumulation is float.
 // fp32 path: one wave per (query, head), plain online softmax.
 #include "xc_internal.h"
 
@@ -27,6 +30,7 @@ namespace xc {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
@@ -44,6 +48,8 @@ __device__ __forceinline__ int row_of_key(int key) {
 }
 
 constexpr int kXcds = 8;
+constexpr int kWaves = 8;            // waves per attention workgroup
+constexpr int kQT = 32 * kWaves;     // queries per attention workgroup
 
 __device__ __forceinline__ float partner_max(float x) {
   // max(x, x of lane ^ 32): v_permlane32_swap exchanges the two half-waves
@@ -57,9 +63,9 @@ __device__ __forceinline__ float partner_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// Work distribution.  An item is (head, 128-query tile); its key tiles are
+// Work distribution.  An item is (head, 256-query tile); its key tiles are
 // split into S equal chunks, S chosen by the launcher so that the units
-// (item, chunk) fill whole rounds of resident workgroups (two per CU).  Units
+// (item, chunk) fill whole rounds of resident workgroups (one per CU).  Units
 // are ordered [head][chunk][query tile] and dealt to the 8 XCDs (each with
 // its own L2) in contiguous ranges (workgroups are dispatched round-robin
 // over the XCDs, so workgroup b takes unit (b mod 8) * per_xcd + b / 8): the
@@ -73,15 +79,16 @@ __device__ __forceinline__ float partner_sum(float x) {
 //   S(j); then O^T += V(j)^T P(j)^T.  K runs one tile ahead of V in LDS:
 //   iteration j reads K(j+1) and V(j) and refills K(j+2) and V(j+1).
 template <int D>
-__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ Kc,
+__global__ __launch_bounds__(64 * kWaves, 1) void attn_bf16_kernel(const bf16* __restrict__ Q, const bf16* __restrict__ Kc,
                                                            const bf16* __restrict__ Vt, bf16* __restrict__ O, int L,
                                                            int Mpad, int Lcap, int Lk, int H, int n_qt, int n_split,
                                                            float sl2, float* __restrict__ ws,
                                                            const int* __restrict__ flag) {
   if (flag != nullptr && *flag) return;
   constexpr int KCH = D / 8;                // 16-byte chunks per key row
-  constexpr int KLD = 64 * KCH / 256;       // K chunks staged per thread
-  constexpr int VLD = D * 8 / 256;          // V^T chunks staged per thread
+  constexpr int NTH = 64 * kWaves;          // threads per workgroup
+  constexpr int KLD = 64 * KCH / NTH;       // K chunks staged per thread
+  constexpr int VLD = D * 8 / NTH;          // V^T chunks staged per thread
   constexpr int DT = D / 32;                // 32-row output tiles (head dims)
   // LDS rows are padded by 16 bytes: the 32 rows a half-wave reads at one
   // chunk position fall in distinct banks, and every fragment address is a
@@ -102,13 +109,14 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* __restric
   const int rem = unit - h * n_split * n_qt;
   const int kc = rem / n_qt, qt = rem - kc * n_qt;
   const int k0 = (int)((long long)kc * NT / n_split), k1 = (int)((long long)(kc + 1) * NT / n_split);
-  const int q0 = qt * 128 + wave * 32;
+  const int q0 = qt * kQT + wave * 32;
 
-  // thread tid stages K rows key0 + (256/KCH) i and V^T rows dd0 + 32 i: one
+  // thread tid stages K rows key0 + KSTEP i and V^T rows dd0 + VSTEP i: one
   // per-thread offset each, the i-steps are wave-uniform (row_of_key maps
-  // key + 16 i to its row + 16 i for key < 16)
-  static_assert(256 / KCH == 16 || 256 / KCH == 32, "staging layout");
-  constexpr int KSTEP = 256 / KCH;
+  // key + 32 i to its row + 32 i for key < 32)
+  constexpr int KSTEP = NTH / KCH;
+  constexpr int VSTEP = NTH / 8;
+  static_assert(KSTEP == 32 || KSTEP == 64, "staging layout");
   const int key0 = tid / KCH, kc0 = tid % KCH;
   const int kg0 = (key0 * D + kc0 * 8) * 2;
   const int ks0 = row_of_key(key0) * KR + kc0 * 8;
@@ -149,7 +157,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* __restric
     auto load_v = [&](int j) __attribute__((always_inline)) {
 #pragma unroll
       for (int i = 0; i < VLD; ++i) {
-        const char* base = Vh + ((long long)i * 32 * Lcap + j * 64) * 2;
+        const char* base = Vh + ((long long)i * VSTEP * Lcap + j * 64) * 2;
         rv[i] = *reinterpret_cast<const u32x4*>(base + vg0);
       }
     };
@@ -159,7 +167,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* __restric
     };
     auto store_v = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
-      for (int i = 0; i < VLD; ++i) *reinterpret_cast<u32x4*>(&sV[buf][vs0 + i * 32 * VR]) = rv[i];
+      for (int i = 0; i < VLD; ++i) *reinterpret_cast<u32x4*>(&sV[buf][vs0 + i * VSTEP * VR]) = rv[i];
     };
     auto qk = [&](f32x16* sacc, int buf) __attribute__((always_inline)) {
 #pragma unroll
@@ -196,20 +204,24 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* __restric
     // (raw score units): p = 2^(s c - m c), c = log2(e)/sqrt(d)
     auto probs = [&](f32x16* sacc, bf16x8* pb) __attribute__((always_inline)) {
       const float msc = -m_run * sl2;
-      float ps = 0.f;
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(sacc[mt][i], sl2, msc));
-          sacc[mt][i] = p;
-          ps += p;
-        }
-      l_run += ps;
+        for (int i = 0; i < 16; ++i) sacc[mt][i] = __builtin_amdgcn_exp2f(fmaf(sacc[mt][i], sl2, msc));
 #pragma unroll
       for (int kv = 0; kv < 4; ++kv)
 #pragma unroll
         for (int i = 0; i < 8; ++i) pb[kv][i] = (bf16)sacc[kv >> 1][(kv & 1) * 8 + i];
+      const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
+      float ps0 = 0.f, ps1 = 0.f;
+#pragma unroll
+      for (int kv = 0; kv < 4; ++kv) {
+        ps0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[kv], pb[kv], 0, 1), ones, ps0, false);
+        ps1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[kv], pb[kv], 2, 3), ones, ps1, false);
+        ps0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[kv], pb[kv], 4, 5), ones, ps0, false);
+        ps1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[kv], pb[kv], 6, 7), ones, ps1, false);
+      }
+      l_run += ps0 + ps1;
     };
     auto pv = [&](const bf16x8* pb, int buf) __attribute__((always_inline)) {
 #pragma unroll
@@ -325,9 +337,9 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* __restric
           }
       }
     } else {
-      // partial: O (unnormalised) [128][D], then running max and sum [128] each
+      // partial: O (unnormalised) [kQT][D], then running max and sum [kQT] each
       const int item = h * n_qt + qt;
-      float* wo = ws + ((long long)item * n_split + kc) * (128 * D + 256);
+      float* wo = ws + ((long long)item * n_split + kc) * (kQT * D + 2 * kQT);
       const int ql = wave * 32 + lo;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
@@ -338,8 +350,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* __restric
           *reinterpret_cast<float4*>(wo + ql * D + dd) = o4;
         }
       if (hi == 0) {
-        wo[128 * D + ql] = m_run;
-        wo[128 * D + 128 + ql] = l_tot;
+        wo[kQT * D + ql] = m_run;
+        wo[kQT * D + kQT + ql] = l_tot;
       }
     }
   }
@@ -356,25 +368,25 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(bf16* __restrict__ O, i
   if (flag != nullptr && *flag) return;
   constexpr int TPQ = D / 16;  // threads per query
   constexpr int QPB = 256 / TPQ;  // queries per workgroup
-  const int blocks_per_item = 128 / QPB;
+  const int blocks_per_item = kQT / QPB;
   const int item = blockIdx.x / blocks_per_item;
   const int ql = (blockIdx.x % blocks_per_item) * QPB + threadIdx.x / TPQ;
   const int d0 = (threadIdx.x % TPQ) * 16;
   const int h = item / n_qt, qt = item - h * n_qt;
-  const int q = qt * 128 + ql;
+  const int q = qt * kQT + ql;
   if (q >= L) return;
-  const long long stride = 128 * D + 256;
+  const long long stride = kQT * D + 2 * kQT;
   const float* base = ws + (long long)item * n_split * stride;
   float M = -INFINITY;
-  for (int p = 0; p < n_split; ++p) M = fmaxf(M, base[p * stride + 128 * D + ql]);
+  for (int p = 0; p < n_split; ++p) M = fmaxf(M, base[p * stride + kQT * D + ql]);
   float acc[16];
 #pragma unroll
   for (int i = 0; i < 16; ++i) acc[i] = 0.f;
   float den = 0.f;
   for (int p = 0; p < n_split; ++p) {
     const float* pp = base + p * stride;
-    const float w = __builtin_amdgcn_exp2f((pp[128 * D + ql] - M) * sl2);
-    den += w * pp[128 * D + 128 + ql];
+    const float w = __builtin_amdgcn_exp2f((pp[kQT * D + ql] - M) * sl2);
+    den += w * pp[kQT * D + kQT + ql];
     const float4* src = reinterpret_cast<const float4*>(pp + ql * D + d0);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -387,6 +399,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(bf16* __restrict__ O, i
   }
   const float inv = 1.0f / den;
   typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
   bf16x8 o0, o1;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
@@ -453,17 +466,18 @@ int resident_attention_groups() {
   if (groups[dev] == 0) {
     int cus = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) cus = 256;
-    groups[dev] = 2 * cus;
+    groups[dev] = cus;
   }
   return groups[dev];
 }
 
 // Key splits per item.  Estimated time in key-tile steps of one resident
 // workgroup: rounds * (tiles per unit + 4 for the unit's prologue and
-// epilogue) + 4 S items / 512 for the merge, over S <= 4 with chunks of at
-// least 4 tiles (fitted to measured split sweeps on the multi-camera shapes).
+// epilogue) + 4 S items / (resident workgroups) for the merge, over S <= 4
+// with chunks of at least 4 tiles (fitted to measured split sweeps on the
+// multi-camera shapes).
 int attention_splits(int L, int Lk, int H) {
-  const int items = H * ((L + 127) / 128);
+  const int items = H * ((L + kQT - 1) / kQT);
   const int NT = (Lk + 63) / 64;
   const int slots = resident_attention_groups();
   int best = 1;
@@ -471,7 +485,7 @@ int attention_splits(int L, int Lk, int H) {
   for (int s = 1; s <= 4 && (s == 1 || NT / s >= 4); ++s) {
     const long long units = (long long)items * s;
     const long long rounds = (units + slots - 1) / slots;
-    const double cost = (double)rounds * ((double)NT / s + 4.0) + (s > 1 ? 4.0 * s * items / 512.0 : 0.0);
+    const double cost = (double)rounds * ((double)NT / s + 4.0) + (s > 1 ? 4.0 * s * items / slots : 0.0);
     if (cost < best_cost - 1e-9) {
       best_cost = cost;
       best = s;
@@ -483,28 +497,28 @@ int attention_splits(int L, int Lk, int H) {
 size_t attention_workspace_floats(int L, int Lk, int H, int D) {
   const int s = attention_splits(L, Lk, H);
   if (s == 1) return 0;
-  return (size_t)H * ((L + 127) / 128) * s * (128 * (size_t)D + 256);
+  return (size_t)H * ((L + kQT - 1) / kQT) * s * (kQT * (size_t)D + 2 * kQT);
 }
 
 // bf16 requirements (checked by the caller): D in {64, 128}; Q has Mpad >=
-// roundup(L, 128) rows per head; the caches have Lcap >= roundup(Lk, 64) rows
+// roundup(L, 256) rows per head; the caches have Lcap >= roundup(Lk, 64) rows
 // whose keys past Lk hold finite values; ws has
 // attention_workspace_floats(L, Lk, H, D) floats.
 void launch_attention(int dtype, const void* q, const void* kc, const void* vt, void* o, float* ws, int L, int Mpad,
                       int Lcap, int Lk, int H, int D, const int* flag, hipStream_t st) {
   if (dtype == 1) {
-    const int n_qt = (L + 127) / 128;
+    const int n_qt = (L + kQT - 1) / kQT;
     const int n_split = attention_splits(L, Lk, H);
     const int units = H * n_split * n_qt;
     const int grid = (units + kXcds - 1) / kXcds * kXcds;
     const float sl2 = 1.4426950408889634f / sqrtf((float)D);
-    const int merge_grid = H * n_qt * (128 / (256 / (D / 16)));
+    const int merge_grid = H * n_qt * (kQT / (256 / (D / 16)));
     if (D == 128) {
-      attn_bf16_kernel<128><<<grid, 256, 0, st>>>((const bf16*)q, (const bf16*)kc, (const bf16*)vt, (bf16*)o, L,
+      attn_bf16_kernel<128><<<grid, 64 * kWaves, 0, st>>>((const bf16*)q, (const bf16*)kc, (const bf16*)vt, (bf16*)o, L,
                                                   Mpad, Lcap, Lk, H, n_qt, n_split, sl2, ws, flag);
       if (n_split > 1) attn_merge_kernel<128><<<merge_grid, 256, 0, st>>>((bf16*)o, L, H, n_qt, n_split, sl2, ws, flag);
     } else {
-      attn_bf16_kernel<64><<<grid, 256, 0, st>>>((const bf16*)q, (const bf16*)kc, (const bf16*)vt, (bf16*)o, L,
+      attn_bf16_kernel<64><<<grid, 64 * kWaves, 0, st>>>((const bf16*)q, (const bf16*)kc, (const bf16*)vt, (bf16*)o, L,
                                                  Mpad, Lcap, Lk, H, n_qt, n_split, sl2, ws, flag);
       if (n_split > 1) attn_merge_kernel<64><<<merge_grid, 256, 0, st>>>((bf16*)o, L, H, n_qt, n_split, sl2, ws, flag);
     }

@@ -688,7 +688,7 @@ xc_status xc_init(const xc_model_config* model, const xc_gate_config* gate, cons
   h->esz = model->dtype == XC_BF16 ? 2 : 4;
   h->L = tokens_of(model);
   // activation rows padded for every GEMM tile height (128, 192, 256) and the
-  // 128-query attention tiles: roundup(L, 256) + 256 >= roundup(L, 192)
+  // 256-query attention tiles: roundup(L, 256) + 256 >= roundup(L, 192)
   h->Mpad = (h->L + 255) / 256 * 256 + 256;
   h->Lcap = ((long long)h->Wkv * h->L + 63) / 64 * 64;
   try {
