@@ -337,8 +337,11 @@ def main():
     L, C = m.tokens, m.hidden
     for k, v in gate_k.items():
         e = {"launches": v["launches"], "avg_us": round(v["avg_us"], 2)}
-        if k == "gate_reduce":
-            e["gbs"] = round(4.0 * L * C / (v["avg_us"] * 1e-6) / 1e9, 1)
+        if k == "gate":
+            # one read of x, the cached fingerprint read and the current one written
+            fp_rows = len(xcp.xc_fingerprint_rows(m, w.gate)) + sum(g.views for g in m.groups)
+            e["bytes"] = 4.0 * L * C + 8.0 * fp_rows * C
+            e["gbs"] = round(e["bytes"] / (v["avg_us"] * 1e-6) / 1e9, 1)
             e["hbm_frac"] = round(e["gbs"] / PEAK_HBM_GBS, 4)
         if k == "skip_add":
             e["note"] = "averaged over launches that add and launches that return at entry"

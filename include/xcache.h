@@ -213,12 +213,14 @@ xc_status xc_fingerprint_rows(const xc_model_config* model, const xc_gate_config
                               int32_t* rows, size_t cap, size_t* n_rows);
 
 /* Kernel timing: while enabled, every launch of the kernel kinds below is
- * bracketed by HIP events on the bound stream. */
+ * bracketed by HIP events on the bound stream.  A gated evaluation is two
+ * launches: XC_KERN_GATE reads the block input once, forms the fingerprint
+ * and compares it with the cached one; XC_KERN_GATE_DECIDE takes the
+ * decision. */
 enum {
   XC_KERN_ATTENTION = 0, XC_KERN_GEMM_QKV = 1, XC_KERN_GEMM_OPROJ = 2, XC_KERN_GEMM_UP = 3,
-  XC_KERN_GEMM_DOWN = 4, XC_KERN_GATE_REDUCE = 5, XC_KERN_GATE_COMPARE = 6, XC_KERN_GATE_DECIDE = 7,
-  XC_KERN_SKIP_ADD = 8, XC_KERN_LN_MOD = 9, XC_KERN_QK_NORM = 10, XC_KERN_ADALN = 11,
-  XC_KERN_COUNT = 12
+  XC_KERN_GEMM_DOWN = 4, XC_KERN_GATE = 5, XC_KERN_GATE_DECIDE = 6, XC_KERN_SKIP_ADD = 7, XC_KERN_LN_MOD = 8,
+  XC_KERN_QK_NORM = 9, XC_KERN_ADALN = 10, XC_KERN_COUNT = 11
 };
 xc_status xc_profile(xc_handle* h, int32_t enable);
 

@@ -66,7 +66,7 @@ struct xc_handle {
   float* cond = nullptr; float* mod = nullptr;
   void* hbuf = nullptr; float* qkv = nullptr; void* q = nullptr; void* o = nullptr; void* u = nullptr;
   float* x1 = nullptr; float* xa = nullptr; float* xb = nullptr;
-  float* fp_partial = nullptr; double* fp_records = nullptr;
+  double* fp_records = nullptr;
   float* attn_ws = nullptr;
   // fingerprint tables
   FpTables tables{};
@@ -437,19 +437,15 @@ xc_status check_launch() {
 
 void build_tables(xc_handle* h) {
   const xc_model_config* m = &h->m;
-  std::vector<int4> chunks;
-  std::vector<int> cam_chunk_begin{0}, cam_tokens, grp_cam_begin{0};
+  std::vector<int> cam_row_begin{0}, grp_cam_begin{0};
   long long start = 0;
   int cam = 0;
   for (int gi = 0; gi < m->n_groups; ++gi) {
     const xc_view_group& vg = m->groups[gi];
     const int T = vg.frames * vg.height * vg.width;
     for (int v = 0; v < vg.views; ++v, ++cam) {
-      for (int r = 0; r < T; r += kFpChunkRows)
-        chunks.push_back(make_int4((int)(start + r), std::min(kFpChunkRows, T - r), cam, 0));
-      cam_chunk_begin.push_back((int)chunks.size());
-      cam_tokens.push_back(T);
       start += T;
+      cam_row_begin.push_back((int)start);
     }
     grp_cam_begin.push_back(cam);
   }
@@ -462,32 +458,25 @@ void build_tables(xc_handle* h) {
   for (int gi = 0; gi < m->n_groups; ++gi)
     h->spatial_count[gi] = (grp_srow_begin[gi + 1] - grp_srow_begin[gi]) * h->C;
 
-  int4* d_chunks = dalloc_t<int4>(h, chunks.size());
-  int* d_ccb = dalloc_t<int>(h, cam_chunk_begin.size());
-  int* d_ct = dalloc_t<int>(h, cam_tokens.size());
+  int* d_crb = dalloc_t<int>(h, cam_row_begin.size());
   int* d_gsb = dalloc_t<int>(h, grp_srow_begin.size());
   int* d_gcb = dalloc_t<int>(h, grp_cam_begin.size());
   int* d_rows = dalloc_t<int>(h, rows.size());
-  XC_HIP(hipMemcpy(d_chunks, chunks.data(), chunks.size() * sizeof(int4), hipMemcpyHostToDevice));
-  XC_HIP(hipMemcpy(d_ccb, cam_chunk_begin.data(), cam_chunk_begin.size() * 4, hipMemcpyHostToDevice));
-  XC_HIP(hipMemcpy(d_ct, cam_tokens.data(), cam_tokens.size() * 4, hipMemcpyHostToDevice));
+  XC_HIP(hipMemcpy(d_crb, cam_row_begin.data(), cam_row_begin.size() * 4, hipMemcpyHostToDevice));
   XC_HIP(hipMemcpy(d_gsb, grp_srow_begin.data(), grp_srow_begin.size() * 4, hipMemcpyHostToDevice));
   XC_HIP(hipMemcpy(d_gcb, grp_cam_begin.data(), grp_cam_begin.size() * 4, hipMemcpyHostToDevice));
   XC_HIP(hipMemcpy(d_rows, rows.data(), rows.size() * 4, hipMemcpyHostToDevice));
   FpTables& t = h->tables;
-  t.n_chunks = (int)chunks.size();
-  t.chunks = d_chunks;
   t.n_cams = cam;
-  t.cam_chunk_begin = d_ccb;
-  t.cam_tokens = d_ct;
+  t.cam_row_begin = d_crb;
   t.n_groups = m->n_groups;
   t.grp_srow_begin = d_gsb;
   t.grp_cam_begin = d_gcb;
   t.n_srows = h->n_srows;
   t.srows = d_rows;
-  h->fp_partial = dalloc_t<float>(h, (size_t)t.n_chunks * h->C);
-  h->n_wg = fp_compare_groups_of_wg(h->C, h->n_srows, h->n_cams);
+  h->n_wg = gate_workgroups(h->C, h->n_srows, h->n_cams);
   h->fp_records = dalloc_t<double>(h, (size_t)h->n_wg * kMaxGroups * kFpRecord);
+
 }
 
 void reset_state(xc_handle* h) {
@@ -736,20 +725,16 @@ xc_status xc_forward_chunk(xc_handle* h, int32_t step, float timestep, const flo
       if (gateable(h, b)) {
         const size_t sb = (size_t)step * h->B + b;
         rhat_tb = wptr<void>(h->rhat, sb * h->L * h->C, h->esz);
-        {
-          Prof p(h, XC_KERN_GATE_REDUCE);
-          launch_fp_colsum(x, h->C, h->tables, h->fp_partial, h->st);
-        }
-        {
-          Prof p(h, XC_KERN_GATE_COMPARE);
-          const size_t fo = sb * h->fp_rows * h->C;
-          launch_fp_compare(x, h->C, h->tables, h->fp_partial, h->fp + fo, h->fp_alt ? h->fp_alt + fo : nullptr,
-                            h->fp_sel ? h->fp_sel + sb : nullptr, h->fp_records, h->st);
-        }
         const bool evaluate = !forced_all && h->visited[sb];
         {
+          Prof p(h, XC_KERN_GATE);
+          const size_t fo = sb * h->fp_rows * h->C;
+          launch_fp_compare(x, h->C, h->tables, h->fp + fo, h->fp_alt ? h->fp_alt + fo : nullptr,
+                            h->fp_sel ? h->fp_sel + sb : nullptr, h->fp_records, h->st);
+        }
+        {
           Prof p(h, XC_KERN_GATE_DECIDE);
-          launch_gate_decide(h->fp_records, h->n_wg, ga, gs, (int)sb, b, h->B, evaluate ? 1 : 0, h->st);
+          launch_gate_decide(h->fp_records, h->n_wg, ga, gs, (int)sb, b, evaluate ? 1 : 0, h->st);
         }
         h->visited[sb] = 1;
         if (evaluate) {

@@ -14,11 +14,9 @@ constexpr int kMaxGroups = 8;
 constexpr int kMaxCond = 512;
 constexpr int kMaxAction = 64;
 
-// Rows per partial column-sum chunk of the fingerprint's global channel.
-constexpr int kFpChunkRows = 16;
-// Columns per workgroup of the fingerprint comparison kernel.
+// Columns per workgroup of the gate kernel.
 constexpr int kFpCompareCols = 32;
-// Doubles per (workgroup, group) partial record of the comparison kernel.
+// Doubles per (workgroup, group) partial record of the gate kernel.
 constexpr int kFpRecord = 8;
 
 // GEMM epilogue modes.
@@ -78,11 +76,8 @@ struct GateState {
 
 // Fingerprint tables (device).
 struct FpTables {
-  int n_chunks;              // partial column-sum chunks
-  const int4* chunks;        // {row_start, n_rows, camera, 0}
   int n_cams;
-  const int* cam_chunk_begin;  // [n_cams + 1] prefix of chunks per camera
-  const int* cam_tokens;     // [n_cams]
+  const int* cam_row_begin;  // [n_cams + 1] first token row of each camera (prefix)
   int n_groups;
   const int* grp_srow_begin; // [G + 1] spatial fingerprint rows per group (prefix)
   const int* grp_cam_begin;  // [G + 1] cameras per group (prefix)
@@ -111,16 +106,17 @@ void launch_skip_add(int dtype, const float* x, const void* rhat, float* out, lo
                      hipStream_t st);
 void launch_axpby(float a, const float* x, float b, const float* y, float* out, long long n, hipStream_t st);
 void launch_pass_begin(const GateState& gs, int n_blocks, hipStream_t st);
-void launch_fp_colsum(const float* x, int C, const FpTables& t, float* partial, hipStream_t st);
-// fp0 / fp1: the (t, b) fingerprint sets; with sel == null the cached
-// fingerprint is fp0 and is overwritten in place, otherwise it is fp[*sel] and
-// the current one goes to the other set.
-void launch_fp_compare(const float* x, int C, const FpTables& t, const float* partial, float* fp0, float* fp1,
-                       const int* sel, double* records, hipStream_t st);
-// Partial records written by the comparison kernel (per group each).
-int fp_compare_groups_of_wg(int C, int n_srows, int n_cams);
-void launch_gate_decide(const double* records, int n_wg, const GateArgs& ga, const GateState& gs, int S_idx,
-                        int b, int n_blocks, int evaluate, hipStream_t st);
+// Gated evaluation, first launch: fingerprint of x against the (t, b) cache
+// and the refresh.  fp0 / fp1: the (t, b) fingerprint sets; with sel == null
+// the cached fingerprint is fp0 and is overwritten in place, otherwise it is
+// fp[*sel] and the current one goes to the other set.  records:
+// gate_workgroups(...) * kMaxGroups * kFpRecord doubles.
+int gate_workgroups(int C, int n_srows, int n_cams);
+void launch_fp_compare(const float* x, int C, const FpTables& t, float* fp0, float* fp1, const int* sel,
+                       double* records, hipStream_t st);
+// Second launch: the decision from the records of the first.
+void launch_gate_decide(const double* records, int n_wg, const GateArgs& ga, const GateState& gs, int sb, int b,
+                        int evaluate, hipStream_t st);
 void launch_fill_f32(float* p, float v, long long n, hipStream_t st);
 
 }  // namespace xc

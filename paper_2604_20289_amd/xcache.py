@@ -27,11 +27,11 @@ XC_FORCE_FULL = 1
 XC_DEC_COMPUTE, XC_DEC_SKIP, XC_DEC_FORCED, XC_DEC_NONE = 0, 1, 2, 255
 XC_MAX_GROUPS = 8
 (XC_KERN_ATTENTION, XC_KERN_GEMM_QKV, XC_KERN_GEMM_OPROJ, XC_KERN_GEMM_UP, XC_KERN_GEMM_DOWN,
- XC_KERN_GATE_REDUCE, XC_KERN_GATE_COMPARE, XC_KERN_GATE_DECIDE, XC_KERN_SKIP_ADD, XC_KERN_LN_MOD,
- XC_KERN_QK_NORM, XC_KERN_ADALN, XC_KERN_COUNT) = range(13)
+ XC_KERN_GATE, XC_KERN_GATE_DECIDE, XC_KERN_SKIP_ADD, XC_KERN_LN_MOD, XC_KERN_QK_NORM, XC_KERN_ADALN,
+ XC_KERN_COUNT) = range(12)
 
-KERNEL_NAMES = ["attention", "gemm_qkv", "gemm_oproj", "gemm_up", "gemm_down", "gate_reduce",
-                "gate_compare", "gate_decide", "skip_add", "ln_mod", "qk_norm", "adaln"]
+KERNEL_NAMES = ["attention", "gemm_qkv", "gemm_oproj", "gemm_up", "gemm_down", "gate", "gate_decide", "skip_add",
+                "ln_mod", "qk_norm", "adaln"]
 
 EXPORTED = ["xc_status_string", "xc_init", "xc_forward_chunk", "xc_kv_update", "xc_stats", "xc_reset",
             "xc_destroy", "xc_axpby", "xc_fingerprint_rows", "xc_profile", "xc_kernel_times"]
