@@ -51,6 +51,11 @@ constexpr int kXcds = 8;
 constexpr int kWaves = 8;            // waves per attention workgroup
 constexpr int kQT = 32 * kWaves;     // queries per attention workgroup
 
+// Workspace floats of one (item, key split) piece: the piece's output
+// normalised by its own softmax sum, bf16 [kQT][D], then its running max and
+// sum, float [kQT] each.
+__host__ __device__ constexpr long long piece_floats(int D) { return (long long)kQT * D / 2 + 2 * kQT; }
+
 __device__ __forceinline__ float partner_max(float x) {
   // max(x, x of lane ^ 32): v_permlane32_swap exchanges the two half-waves
   // (a VALU operation, no LDS round trip)
@@ -337,28 +342,34 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_bf16_kernel(const bf16* _
           }
       }
     } else {
-      // partial: O (unnormalised) [kQT][D], then running max and sum [kQT] each
+      // partial piece (see piece_floats)
       const int item = h * n_qt + qt;
-      float* wo = ws + ((long long)item * n_split + kc) * (kQT * D + 2 * kQT);
+      float* wo = ws + ((long long)item * n_split + kc) * piece_floats(D);
+      bf16* wob = reinterpret_cast<bf16*>(wo);
       const int ql = wave * 32 + lo;
+      const float inv = 1.0f / l_tot;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int dd = dt * 32 + g * 8 + hi * 4;
-          float4 o4 = {oacc[dt][g * 4], oacc[dt][g * 4 + 1], oacc[dt][g * 4 + 2], oacc[dt][g * 4 + 3]};
-          *reinterpret_cast<float4*>(wo + ql * D + dd) = o4;
+          typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+          bf16x4 o4;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) o4[r] = (bf16)(oacc[dt][g * 4 + r] * inv);
+          *reinterpret_cast<bf16x4*>(wob + ql * D + dd) = o4;
         }
       if (hi == 0) {
-        wo[kQT * D + ql] = m_run;
-        wo[kQT * D + kQT + ql] = l_tot;
+        wo[kQT * D / 2 + ql] = m_run;
+        wo[kQT * D / 2 + kQT + ql] = l_tot;
       }
     }
   }
 }
 
 // Combines the S pieces of each item in a fixed order (deterministic):
-// O = sum_p 2^((m_p - M) c) O_p / sum_p 2^((m_p - M) c) l_p, M = max_p m_p.
+// O = sum_p w_p l_p Ohat_p / sum_p w_p l_p, w_p = 2^((m_p - M) c),
+// M = max_p m_p, Ohat_p the piece's normalised output.
 // One workgroup per 32 queries of an item; a thread owns one query and 16
 // consecutive head dims.
 template <int D>
@@ -375,31 +386,27 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(bf16* __restrict__ O, i
   const int h = item / n_qt, qt = item - h * n_qt;
   const int q = qt * kQT + ql;
   if (q >= L) return;
-  const long long stride = kQT * D + 2 * kQT;
+  const long long stride = piece_floats(D);
   const float* base = ws + (long long)item * n_split * stride;
   float M = -INFINITY;
-  for (int p = 0; p < n_split; ++p) M = fmaxf(M, base[p * stride + kQT * D + ql]);
+  for (int p = 0; p < n_split; ++p) M = fmaxf(M, base[p * stride + kQT * D / 2 + ql]);
   float acc[16];
 #pragma unroll
   for (int i = 0; i < 16; ++i) acc[i] = 0.f;
   float den = 0.f;
   for (int p = 0; p < n_split; ++p) {
     const float* pp = base + p * stride;
-    const float w = __builtin_amdgcn_exp2f((pp[kQT * D + ql] - M) * sl2);
-    den += w * pp[kQT * D + kQT + ql];
-    const float4* src = reinterpret_cast<const float4*>(pp + ql * D + d0);
+    const float w = __builtin_amdgcn_exp2f((pp[kQT * D / 2 + ql] - M) * sl2) * pp[kQT * D / 2 + kQT + ql];
+    den += w;
+    const bf16x8* src = reinterpret_cast<const bf16x8*>(reinterpret_cast<const bf16*>(pp) + ql * D + d0);
+    const bf16x8 v0 = src[0], v1 = src[1];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float4 v = src[i];
-      acc[4 * i] += w * v.x;
-      acc[4 * i + 1] += w * v.y;
-      acc[4 * i + 2] += w * v.z;
-      acc[4 * i + 3] += w * v.w;
+    for (int i = 0; i < 8; ++i) {
+      acc[i] += w * (float)v0[i];
+      acc[8 + i] += w * (float)v1[i];
     }
   }
   const float inv = 1.0f / den;
-  typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
   bf16x8 o0, o1;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
@@ -497,7 +504,7 @@ int attention_splits(int L, int Lk, int H) {
 size_t attention_workspace_floats(int L, int Lk, int H, int D) {
   const int s = attention_splits(L, Lk, H);
   if (s == 1) return 0;
-  return (size_t)H * ((L + kQT - 1) / kQT) * s * (kQT * (size_t)D + 2 * kQT);
+  return (size_t)H * ((L + kQT - 1) / kQT) * s * (size_t)piece_floats(D);
 }
 
 // bf16 requirements (checked by the caller): D in {64, 128}; Q has Mpad >=
