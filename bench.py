@@ -48,8 +48,8 @@ PEAK_HBM_GBS = 8000.0
 # scaled by a 512 MiB copy-kernel calibration; valid only for the kernel
 # source they were taken on (sha1 prefix of the file).
 MEASURED_TRAFFIC = {
-    "attention": {"source": "paper_2604_20289_amd/csrc/xc_attention.hip", "sha1": "a39a672cb825f0fd",
-                  "bytes": (523.8 + 153.4) * 1e6},
+    "attention": {"source": "paper_2604_20289_amd/csrc/xc_attention.hip", "sha1": "fb0e43f08a8bac04",
+                  "bytes": (358.8 + 89.7) * 1e6},
 }
 
 
