@@ -155,6 +155,37 @@ def cpu_baseline(w, weights, seed):
                        f"chunk")}
 
 
+def ablations(w, m, weights, eps_dev, actions, stream, args, xcp, torch):
+    """Synthetic analogues of the paper's gate ablations (Section 4.4): the same stream under
+    step-0 handling, anchor, staleness, refresh and threshold variants; skip rate and latency only."""
+    variants = [
+        ("table1", {}),
+        ("step0_force", {"step0_mode": xcp.XC_STEP0_FORCE}),
+        ("step0_strict", {"step0_mode": xcp.XC_STEP0_STRICT}),
+        ("front_anchors_0", {"front_anchors": 0}),
+        ("back_anchors_1", {"back_anchors": 1}),
+        ("max_stale_1", {"max_stale": 1}),
+        ("fp_refresh_on_compute", {"fp_refresh": xcp.XC_FP_REFRESH_ON_COMPUTE}),
+        ("fixed_tau_0.97", {"adaptive": 0, "tau_cos_fixed": 0.97}),
+    ] + [(f"tau_floor_{tf:.2f}", {"tau_floor": tf}) for tf in (0.93, 0.95, 0.96, 0.97, 0.98, 0.99)]
+    out = {"metric": "gate ablations: block skip rate and gate-on chunk latency", "workload": w.name,
+           "warmup": args.warmup, "steps": args.steps, "data": "synthetic", "variants": {}}
+    B, S = m.n_blocks, m.n_steps
+    for name, kw in variants:
+        wv = synth.with_gate(w, **kw)
+        xc = xcp.XCache(m, wv.gate, weights, stream)
+        ms = [v[0] for v in run_stream(xc, m, eps_dev, actions, args.warmup, args.steps, torch)]
+        st = xc.stats()
+        xc.close()
+        per_block = np.asarray(st["skip_counts"]).reshape(S, B).sum(axis=0).astype(int).tolist()
+        out["variants"][name] = {"gate": kw, "skip_rate": round(st["skips"] / max(1, st["evals_post_warmup"]), 4),
+                                 "mean_ms": round(statistics.mean(ms), 3),
+                                 "median_ms": round(statistics.median(ms), 3),
+                                 "skips_per_block": per_block}
+        log(f"ablation {name}: skip rate {out['variants'][name]['skip_rate']}, {out['variants'][name]['mean_ms']} ms")
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -169,6 +200,10 @@ def main():
     ap.add_argument("--force-every", type=int, default=0,
                     help="also run the gate-on stream with every P-th generation computed in full and report "
                          "the per-chunk skip fractions (the paper's periodic refresh cadence)")
+    ap.add_argument("--ablations", action="store_true",
+                    help="instead of the benchmark line, print one line of gate ablations on the same stream: "
+                         "step-0 modes, anchors, staleness bound, refresh mode and a tau_floor sweep (skip rate "
+                         "and mean chunk latency of each; --steps timed chunks after --warmup)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="copy a buffer of this many MiB once (calibrates rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     args = ap.parse_args()
@@ -208,6 +243,10 @@ def main():
         torch.cuda.synchronize()
         log(f"calibration copy of {args.calib_copy_mib} MiB done")
         del src, dst
+
+    if args.ablations:
+        print(json.dumps(ablations(w, m, weights, eps_dev, actions, stream, args, xcp, torch)), flush=True)
+        return
 
     # 1. gate on
     xc = xcp.XCache(m, w.gate, weights, stream)

@@ -53,6 +53,10 @@ CFG0_VARIANTS = {
         synth.with_gate(W0, adaptive=1, tau_floor=0.97, tau_dev=2.0, back_anchors=1), n_blocks=4), rho=0.999),
     "refresh-on-compute": synth.with_stream(synth.with_gate(W0, adaptive=1, tau_floor=0.97, tau_dev=2.0,
                                                             fp_refresh=xo.FP_REFRESH_ON_COMPUTE), rho=0.999),
+    # the gate-stress stream's mechanisms at the tiny shape: an i.i.d. redraw every 3rd chunk (scene
+    # cut) and a large action step every 2nd chunk, over an otherwise slowly varying stream
+    "scene-cut-steer": synth.with_stream(synth.with_gate(W0, adaptive=1, tau_floor=0.9, tau_dev=2.0),
+                                         rho=0.999, cut_every=3, big_every=2, big_sigma=1.0, n_chunks=7),
     "gate-off": synth.with_gate(W0, enabled=0),
     "window-1": synth.with_stream(synth.with_model(synth.with_gate(W0, adaptive=1, tau_floor=0.9, tau_dev=2.0),
                                                    kv_window=1), rho=0.999),
@@ -70,6 +74,8 @@ def test_cfg0_variants(name):
             assert st["skips"] == 0
         if name == "always-skip":
             assert st["skips"] == 5 * 4 * 1   # 5 post-warmup chunks x 4 steps x 1 gated block
+        if name == "scene-cut-steer":
+            assert st["skips"] > 0
     finally:
         ls.close()
 
