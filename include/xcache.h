@@ -182,7 +182,9 @@ xc_status xc_forward_chunk(xc_handle* h, int32_t step, float timestep, const flo
  * kv_window - 1 past chunks are kept), the action remembered for the next
  * generation's action channel, then n <- n + 1.  Never gated.
  *   x_clean : device float32 [L, C].
- *   x_out   : device float32 [L, C] or NULL (output not needed). */
+ *   x_out   : device float32 [L, C], or NULL when the pass's output is not
+ *             needed: the last block then stops after its key/value
+ *             projection (its attention and MLP feed nothing else). */
 xc_status xc_kv_update(xc_handle* h, float timestep, const float* action_host,
                        const void* x_clean, void* x_out);
 

@@ -331,8 +331,10 @@ P* wptr(void* base, size_t elems_before, size_t esz) {
 // QKV projection, QK-norm and cache write, attention over the visible window,
 // output projection with gated residual, LN+modulate, MLP up with GELU, MLP
 // down with gated residual and (for gated blocks) the cached-residual store.
+// kv_only: stop after the key/value cache write (the block's output is not
+// needed: the last block of a KV-update pass whose caller takes no output).
 void compute_block(xc_handle* h, int b, const float* x, float* out, const int* flag, void* rhat_tb,
-                   long long kv_off, long long Lk) {
+                   long long kv_off, long long Lk, bool kv_only = false) {
   const int C = h->C, H = h->H, D = h->D, Dm = h->Dm;
   const int L = (int)h->L;
   const size_t esz = h->esz;
@@ -379,6 +381,7 @@ void compute_block(xc_handle* h, int b, const float* x, float* out, const int* f
     launch_qk_norm(h->dtype, h->qkv, h->gq + (size_t)b * D, h->gk + (size_t)b * D, h->q, kc_b, vt_b, L, H, D,
                    (int)h->Mpad, (int)h->Lcap, (int)kv_off, flag, h->st);
   }
+  if (kv_only) return;
   {
     Prof p(h, XC_KERN_ATTENTION);
     launch_attention(h->dtype, h->q, kc_b, vt_b, h->o, h->attn_ws, L, (int)h->Mpad, (int)h->Lcap, (int)Lk, H, D, flag,
@@ -773,7 +776,7 @@ xc_status xc_kv_update(xc_handle* h, float timestep, const float* action_host, c
     for (int b = 0; b < h->B; ++b) {
       float* out = (b & 1) ? h->xb : h->xa;
       if (b == h->B - 1 && x_out) out = reinterpret_cast<float*>(x_out);
-      compute_block(h, b, x, out, nullptr, nullptr, kv_off, Lk);
+      compute_block(h, b, x, out, nullptr, nullptr, kv_off, Lk, b == h->B - 1 && !x_out);
       x = out;
     }
     h->kv_block_evals += h->B;

@@ -90,6 +90,18 @@ def test_cfg0_force_full_every_other_chunk():
         ls.close()
 
 
+def test_kv_update_without_output():
+    """No output buffer for the KV-update pass: the last block stops after its
+    key/value projection, and every later pass still matches the oracle (fp32
+    and bf16, the last block gated in both)."""
+    for w, kw in ((CFG0_VARIANTS["table1-rho0.999"], dict(tol_abs=TOL32)), (BF_RAGGED, dict(tol_rel_l2=TOLBF))):
+        ls = _ls(w)
+        try:
+            ls.run(4, kv_out=False, **kw)
+        finally:
+            ls.close()
+
+
 def test_cfg0_natural_skips_happen():
     ls = _ls(CFG0_VARIANTS["table1-rho0.999"])
     try:
