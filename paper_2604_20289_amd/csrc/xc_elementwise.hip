@@ -52,29 +52,70 @@ __global__ void cond_kernel(CondArgs a, int temb_dim, int action_dim, float time
   }
 }
 
-// mod[blk][r] = sum_j W_ada[blk][r][j] * cond_silu[j] + b_ada[blk][r]: one wave
-// per output row, lanes striding the conditioning vector (coalesced rows).
+// mod[blk][r] = sum_j W_ada[blk][r][j] * cond_silu[j] + b_ada[blk][r].  A wave
+// takes 8 consecutive output rows and issues all their 16-byte weight loads
+// before any arithmetic (lane l reads elements [V l, V l + V) of each row, V =
+// 16 / sizeof(T); when V does not divide the row length the rows go
+// element-wise), then reduces the 8 dot products across the wave.
 template <typename T>
 __global__ __launch_bounds__(256) void adaln_kernel(const T* __restrict__ w, const float* __restrict__ b,
                                                     const float* __restrict__ cond_silu, int rows_per_block,
                                                     long long block_stride_w, long long block_stride_b,
                                                     int n_rows_total, int dc, float* __restrict__ mod) {
+  constexpr int V = 16 / sizeof(T);
+  constexpr int kRowsPerWave = 8;
+  typedef T tvec __attribute__((ext_vector_type(V)));
   __shared__ float s_c[kMaxCond];
   for (int j = threadIdx.x; j < dc; j += blockDim.x) s_c[j] = cond_silu[j];
   __syncthreads();
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  constexpr int kRowsPerWave = 4;
-  int row0 = (blockIdx.x * 4 + wave) * kRowsPerWave;
-  for (int rr = 0; rr < kRowsPerWave; ++rr) {
-    int row = row0 + rr;
-    if (row >= n_rows_total) return;
-    int blk = row / rows_per_block, r = row - blk * rows_per_block;
-    const T* wr = w + blk * block_stride_w + (long long)r * dc;
-    float acc = 0.f;
-    for (int j = lane; j < dc; j += 64) acc += to_f(wr[j]) * s_c[j];
-    acc = wave_sum(acc);
-    if (lane == 0) mod[row] = acc + b[blk * block_stride_b + r];
+  const int row0 = (blockIdx.x * 4 + wave) * kRowsPerWave;
+  // whole 16-byte chunks per row (rows start 16-byte aligned only when V divides dc)
+  const int n_chunks = dc % V == 0 ? dc / V : 0;
+  float acc[kRowsPerWave];
+#pragma unroll
+  for (int rr = 0; rr < kRowsPerWave; ++rr) acc[rr] = 0.f;
+  for (int j0 = 0; j0 < n_chunks; j0 += 64) {
+    const int j = j0 + lane;
+    tvec v[kRowsPerWave];
+#pragma unroll
+    for (int rr = 0; rr < kRowsPerWave; ++rr) {
+      const int row = row0 + rr;
+      if (row < n_rows_total && j < n_chunks) {
+        const int blk = row / rows_per_block, r = row - blk * rows_per_block;
+        v[rr] = *reinterpret_cast<const tvec*>(w + blk * block_stride_w + (long long)r * dc + (long long)j * V);
+      } else {
+#pragma unroll
+        for (int e = 0; e < V; ++e) v[rr][e] = (T)0.f;
+      }
+    }
+    if (j < n_chunks)
+#pragma unroll
+      for (int rr = 0; rr < kRowsPerWave; ++rr)
+#pragma unroll
+        for (int e = 0; e < V; ++e) acc[rr] += to_f(v[rr][e]) * s_c[j * V + e];
+  }
+  for (int jt = n_chunks * V + lane; jt < dc; jt += 64)
+#pragma unroll
+    for (int rr = 0; rr < kRowsPerWave; ++rr) {
+      const int row = row0 + rr;
+      if (row < n_rows_total) {
+        const int blk = row / rows_per_block, r = row - blk * rows_per_block;
+        acc[rr] += to_f(w[blk * block_stride_w + (long long)r * dc + jt]) * s_c[jt];
+      }
+    }
+#pragma unroll
+  for (int rr = 0; rr < kRowsPerWave; ++rr) acc[rr] = wave_sum(acc[rr]);
+  if (lane < kRowsPerWave) {
+    float a = acc[0];
+#pragma unroll
+    for (int rr = 1; rr < kRowsPerWave; ++rr) a = lane == rr ? acc[rr] : a;
+    const int row = row0 + lane;
+    if (row < n_rows_total) {
+      const int blk = row / rows_per_block, r = row - blk * rows_per_block;
+      mod[row] = a + b[blk * block_stride_b + r];
+    }
   }
 }
 
@@ -236,7 +277,7 @@ void launch_adaln(int dtype, const void* w_ada, const float* b_ada, const float*
   // W_ada is [n_blocks][rows_per_block][dc] and b_ada [n_blocks][rows_per_block]:
   // block_stride_w = rows_per_block * dc, the bias stride is rows_per_block.
   int total = rows_per_block * n_blocks;
-  int grid = (total + 15) / 16;
+  int grid = (total + 31) / 32;  // 4 waves x 8 rows
   if (dtype == 1)
     adaln_kernel<bf16><<<grid, 256, 0, st>>>((const bf16*)w_ada, b_ada, cond_silu, rows_per_block, block_stride_w,
                                              rows_per_block, total, dc, mod);
