@@ -73,3 +73,65 @@ def test_multicamera_fullsize_two_blocks():
         assert err <= 2e-2
     finally:
         xc.close()
+
+
+def test_large_multicamera_fullsize_one_block():
+    """The larger multi-camera shapes (L = 12096 tokens, hidden 2048, 16 heads x 128, MLP 8192, 7
+    cameras), one gated block (no front anchor): every launch at its full size.  The oracle runs
+    chunk 0 in full (float32 with bf16 storage rounding), then the KV-update pass and chunk 1 step 0
+    (24192 keys) on sampled token rows only (its row-restricted checking mode: keys and values from
+    every token, queries and the rest on the sampled rows).
+
+    Checked: chunk 0 step 0 (warmup) on the sampled rows, the gate's metrics and decision at chunk 1
+    against the oracle's (outside the 1e-3 band), and chunk 1's output on the sampled rows -- both
+    relative L2 2e-2."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from lockstep import in_band, rel_l2
+    from paper_2604_20289_amd.xcache import XCache
+
+    w = synth.with_model(synth.with_gate(synth.workload(3), front_anchors=0), n_blocks=1)
+    m = w.model
+    L = m.tokens
+    cam_starts = np.cumsum([0] + [g.frames * g.height * g.width for g in m.groups for _ in range(g.views)])
+    rows = np.unique(np.concatenate([np.linspace(0, L - 1, 97).astype(int), cam_starts[:-1],
+                                     cam_starts[1:] - 1]))
+    blob = synth.make_weights(m)
+    print(f"[fullsize-large] L={L} C={m.hidden} heads={m.n_heads} rows checked={len(rows)}", flush=True)
+    xc = XCache(m, w.gate, blob, torch.cuda.current_stream().cuda_stream)
+    orc = xo.XCacheOracle(m, w.gate, blob, compute=np.float32)
+    eps = list(synth.latent_stream(m, w.stream, 0, 2))
+    acts = list(synth.action_stream(m, w.stream, 0, 2))
+    taus = synth.timesteps(m)
+    try:
+        dev = torch.device("cuda")
+        y = torch.empty((L, m.hidden), dtype=torch.float32, device=dev)
+        xc.forward_chunk(0, taus[0], acts[0], torch.from_numpy(eps[0]).to(dev), y)
+        yo = orc.forward_chunk(0, taus[0], acts[0], eps[0])
+        err = rel_l2(y.cpu().numpy()[rows], yo[rows])
+        print(f"[fullsize-large] chunk 0 step 0 rel-L2 on sampled rows {err:.2e}", flush=True)
+        assert err <= 2e-2
+        # KV-update pass, each side on its own chunk-0 output (the device takes no output buffer)
+        xc.kv_update(0.0, acts[0], y)
+        orc.kv_update(0.0, acts[0], yo, rows=rows)
+        xc.forward_chunk(0, taus[0], acts[1], torch.from_numpy(eps[1]).to(dev), y)
+        st = xc.stats()
+
+        def decide(b, info):
+            dev_skip = int(st["last_decision"][b]) == xo.DEC_SKIP
+            if dev_skip != bool(info["skip"]):
+                assert in_band(info, w.gate.tau_dev), (b, info, st["last_cos"][b], st["last_dev"][b])
+            return dev_skip
+
+        yo1 = orc.forward_chunk(0, taus[0], acts[1], eps[1], decide=decide, rows=rows)
+        info = orc.last[0]
+        print(f"[fullsize-large] chunk 1 gate: oracle s={info['s']:.6f} d={info['d']:.4f} tau={info['tau']:.4f}; "
+              f"device s={st['last_cos'][0]:.6f} d={st['last_dev'][0]:.4f} decision={st['last_decision'][0]}",
+              flush=True)
+        assert abs(st["last_cos"][0] - info["s"]) < 1e-3
+        assert abs(st["last_dev"][0] - info["d"]) < 1e-2 * max(1.0, info["d"])
+        err = rel_l2(y.cpu().numpy()[rows], yo1)
+        print(f"[fullsize-large] chunk 1 step 0 rel-L2 on sampled rows {err:.2e}", flush=True)
+        assert err <= 2e-2
+    finally:
+        xc.close()

@@ -315,3 +315,29 @@ def test_skip_rate_denominator_counts_all_blocks_after_warmup():
     assert orc.evals_post_warmup == B * S * 4
     assert orc.skips == sum(1 for n, t, r in rec for x in r if x["decision"] == xo.DEC_SKIP)
     assert orc.skips > 0
+
+
+def test_row_restricted_checking_mode():
+    """The oracle's row-restricted mode returns exactly the selected rows of the full computation
+    (a block's output row depends on the other tokens only through keys and values)."""
+    w = synth.with_stream(synth.with_gate(synth.workload(0), adaptive=1, tau_floor=0.9, tau_dev=2.0), rho=0.999)
+    m = w.model
+    blob = synth.make_weights(m)
+    rows = np.array([0, 5, 17, 33, 63])
+    full = xo.XCacheOracle(m, w.gate, blob)
+    part = xo.XCacheOracle(m, w.gate, blob)
+    taus = synth.timesteps(m)
+    for n, (eps, a) in enumerate(zip(synth.latent_stream(m, w.stream, 0, 3), synth.action_stream(m, w.stream, 0, 3))):
+        y_full = full.forward_chunk(0, taus[0], a, eps)
+        y_part = part.forward_chunk(0, taus[0], a, eps, rows=rows)
+        np.testing.assert_allclose(y_part, y_full[rows], rtol=1e-12, atol=1e-12)
+        assert [i["decision"] for i in full.last] == [i["decision"] for i in part.last]
+        # the restricted pass left the last block's residual cache alone: continue both on the full path
+        part.rhat = {k: v.copy() for k, v in full.rhat.items()}
+        k_full = full.kv_update(0.0, a, y_full)
+        k_part = part.kv_update(0.0, a, y_full, rows=rows)
+        np.testing.assert_allclose(k_part, k_full[rows], rtol=1e-12, atol=1e-12)
+        for b in range(m.n_blocks):
+            for (k1, v1), (k2, v2) in zip(full.ring[b], part.ring[b]):
+                np.testing.assert_array_equal(k1, k2)
+                np.testing.assert_array_equal(v1, v2)
