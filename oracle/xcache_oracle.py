@@ -25,6 +25,13 @@ The DiT block itself is not specified by the paper beyond adaLN-Zero
 conditioning on timestep and action (Sections 1 and 2.3.2); the block below is
 a standard adaLN DiT block (LayerNorm without affine, six-way modulation,
 QK-RMSNorm, softmax self-attention over the rolling cache, tanh-GELU MLP).
+Two optional extensions move it toward the WAN-style blocks of the paper's
+model (built on WAN 2.2, Section 3.1): a 3-D rotary position embedding of the
+self-attention queries and keys over the latent (frame, row, column) grid,
+with absolute frame positions across chunks, applied before the keys enter the
+cache; and a cross-attention layer between the self-attention and the MLP that
+attends to a condition token sequence (the text / object / lane embeddings the
+paper injects through cross-attention, Sections 2.1 and 2.3.2).
 
 Precision.  Arithmetic is float64.  For a bf16 model (the paper runs its DiT in
 BF16, Section 3.1.1) values are rounded to bf16 (round to nearest even) at the
@@ -115,6 +122,55 @@ def timestep_embedding(tau: float, dim: int) -> np.ndarray:
     h = dim // 2
     f = np.exp(-math.log(10000.0) * np.arange(h, dtype=np.float64) / h)
     return np.concatenate([np.cos(tau * f), np.sin(tau * f)])
+
+
+def rope_axis_dims(d: int) -> Tuple[int, int, int]:
+    """Head dimensions given to the (frame, row, column) axes of the 3-D rotary
+    embedding: the row and column axes get 2 floor(d/6) each, the frame axis
+    the rest (the split of WAN-style 3-D RoPE)."""
+    s = d // 6
+    return d - 4 * s, 2 * s, 2 * s
+
+
+def rope_pair_frequencies(d: int, theta: float) -> Tuple[np.ndarray, np.ndarray]:
+    """For each of the d/2 rotated pairs (2j, 2j+1) of a head: the axis it
+    follows (0 frame, 1 row, 2 column) and its angular frequency theta^(-2i/d_a),
+    i the pair's index within its axis's d_a/2 pairs."""
+    axes, omega = [], []
+    for a, da in enumerate(rope_axis_dims(d)):
+        for i in range(da // 2):
+            axes.append(a)
+            omega.append(theta ** (-2.0 * i / da))
+    return np.asarray(axes, dtype=np.int64), np.asarray(omega, dtype=np.float64)
+
+
+def token_positions(groups: Sequence[synth.ViewGroup], n: int) -> np.ndarray:
+    """[L, 3] positions (n F + f, h, w) of generation n's tokens: camera-major,
+    each camera's (f, h, w) grid row-major; the frame position is absolute
+    across chunks (F frames per chunk), so keys cached from earlier chunks keep
+    their own frame positions."""
+    out = []
+    for g in groups:
+        for _v in range(g.views):
+            for f in range(g.frames):
+                for hh in range(g.height):
+                    for ww in range(g.width):
+                        out.append((n * g.frames + f, hh, ww))
+    return np.asarray(out, dtype=np.float64)
+
+
+def apply_rope(x: np.ndarray, pos: np.ndarray, theta: float) -> np.ndarray:
+    """Rotate each pair (x[2j], x[2j+1]) of every head by the angle p_a omega_j,
+    p_a the token's position on the pair's axis: x [L, H, d], pos [L, 3]."""
+    axes, omega = rope_pair_frequencies(x.shape[-1], theta)
+    ang = pos[:, axes] * omega
+    c = np.cos(ang)[:, None, :]
+    s = np.sin(ang)[:, None, :]
+    a, b = x[..., 0::2], x[..., 1::2]
+    out = np.empty_like(x)
+    out[..., 0::2] = a * c - b * s
+    out[..., 1::2] = a * s + b * c
+    return out
 
 
 def softmax_attention(q, k, v):
@@ -259,7 +315,7 @@ def skip_rule(g: synth.GateParams, s: float, d: float, tau: float, stale: int) -
 class BlockWeights:
     def __init__(self, m: synth.ModelShape, blob: np.ndarray, b: int, compute=np.float64):
         t = synth.split_block_weights(m, blob, b)
-        lin = ("w_ada", "wq", "wk", "wv", "wo", "w1", "w2")
+        lin = ("w_ada", "wq", "wk", "wv", "wo", "w1", "w2", "wq_c", "wk_c", "wv_c", "wo_c")
         self.p = {}
         for name, a in t.items():
             a = np.asarray(a, dtype=np.float64)
@@ -284,7 +340,26 @@ class XCacheOracle:
         self.bf16 = model.dtype == synth.BF16
         self.blocks = [BlockWeights(model, weights, b, compute) for b in range(model.n_blocks)]
         self.rows = fingerprint_rows(model.groups, gate.fp_budget, gate.fp_mode)
+        self.cross_kv: Optional[List[Tuple[np.ndarray, np.ndarray]]] = None
         self.reset()
+
+    def set_condition(self, cond: np.ndarray):
+        """Condition tokens [n, C] (1 <= n <= cond_len) of the cross-attention
+        layer; each block's keys and values of them are computed here once and
+        used by every later pass until the next call."""
+        m = self.m
+        cond = np.asarray(cond, dtype=np.float64)
+        assert m.cond_len > 0 and cond.ndim == 2 and 1 <= cond.shape[0] <= m.cond_len
+        assert cond.shape[1] == m.hidden
+        n, H, d = cond.shape[0], m.n_heads, m.head_dim
+        cr = self._rnd(cond)
+        self.cross_kv = []
+        for b in range(m.n_blocks):
+            p = self.blocks[b].p
+            k = self._rnd(rms_norm((cr @ p["wk_c"].T + p["bk_c"]).reshape(n, H, d), p["gk_c"]))
+            v = self._rnd((cr @ p["wv_c"].T + p["bv_c"]).reshape(n, H, d))
+            self.cross_kv.append((np.ascontiguousarray(k.transpose(1, 0, 2)),
+                                  np.ascontiguousarray(v.transpose(1, 0, 2))))
 
     # -- state ---------------------------------------------------------------
     def reset(self):
@@ -331,8 +406,14 @@ class XCacheOracle:
         q = h[rows if rows is not None else slice(None)] @ p["wq"].T + p["bq"]
         k = h @ p["wk"].T + p["bk"]
         v = h @ p["wv"].T + p["bv"]
-        q = self._rnd(rms_norm(q.reshape(Lq, H, d), p["gq"]))
-        k = self._rnd(rms_norm(k.reshape(L, H, d), p["gk"]))
+        q = rms_norm(q.reshape(Lq, H, d), p["gq"])
+        k = rms_norm(k.reshape(L, H, d), p["gk"])
+        if m.rope:
+            pos = token_positions(m.groups, self.n)
+            q = apply_rope(q, pos[rows] if rows is not None else pos, m.rope_theta)
+            k = apply_rope(k, pos, m.rope_theta)
+        q = self._rnd(q)
+        k = self._rnd(k)
         v = self._rnd(v.reshape(L, H, d))
         kh = np.ascontiguousarray(k.transpose(1, 0, 2))
         vh = np.ascontiguousarray(v.transpose(1, 0, 2))
@@ -343,10 +424,29 @@ class XCacheOracle:
             o[:, hd, :] = softmax_attention(q[:, hd, :], kall[hd], vall[hd])
         o = self._rnd(o.reshape(Lq, C))
         x1 = x + g1 * (o @ p["wo"].T + p["bo"])
+        if m.cond_len > 0:
+            x1 = self.cross_attention(b, x1)
         h2 = self._rnd(layer_norm(x1) * (1.0 + sc2) + sh2)
         u = self._rnd(gelu_tanh(h2 @ p["w1"].T + p["b1"]))
         y = x1 + g2 * (u @ p["w2"].T + p["b2"])
         return y, (kh, vh)
+
+    def cross_attention(self, b: int, x1: np.ndarray) -> np.ndarray:
+        """The cross-attention layer of block b on its rows x1 [Lq, C]: affine
+        LayerNorm, q projection with RMSNorm, softmax attention over the
+        condition's keys and values, output projection added to the stream
+        (no adaLN gate)."""
+        m, p = self.m, self.blocks[b].p
+        assert self.cross_kv is not None, "set_condition() first"
+        Lq, C, H, d = x1.shape[0], m.hidden, m.n_heads, m.head_dim
+        kc, vc = self.cross_kv[b]
+        hc = self._rnd(layer_norm(x1) * p["ln3_w"] + p["ln3_b"])
+        qc = self._rnd(rms_norm((hc @ p["wq_c"].T + p["bq_c"]).reshape(Lq, H, d), p["gq_c"]))
+        oc = np.empty((Lq, H, d), dtype=self.compute)
+        for hd in range(H):
+            oc[:, hd, :] = softmax_attention(qc[:, hd, :], kc[hd], vc[hd])
+        oc = self._rnd(oc.reshape(Lq, C))
+        return x1 + (oc @ p["wo_c"].T + p["bo_c"])
 
     def cond(self, tau: float, action: np.ndarray) -> np.ndarray:
         return np.concatenate([timestep_embedding(tau, self.m.temb_dim),

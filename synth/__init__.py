@@ -14,7 +14,10 @@ chunk, Section 3.1):
 
 * weights: every Linear weight and bias ~ N(0, 0.02^2), drawn row-major
   [out, in] per block in the blob order below from ``default_rng(seed)``;
-  QK-norm gains are 1.
+  QK-norm gains are 1; the cross-attention LayerNorm (models with a
+  cross-attention layer) has scale 1 + N(0, 0.02^2) and shift N(0, 0.02^2).
+* cross-attention condition (models that have one): [n_tokens, C] ~ N(0, 1)
+  from ``default_rng(seed + 3)``.
 * latent noise: eps_0 ~ N(0, I); eps_n = rho * eps_{n-1} + sqrt(1 - rho^2) z_n,
   from ``default_rng(seed + 1)``; optionally redrawn i.i.d. every ``cut_every``
   chunks (scene cut).
@@ -68,6 +71,9 @@ class ModelShape:
     n_steps: int
     kv_window: int          # chunks visible to attention, the current one included
     groups: Tuple[ViewGroup, ...]
+    rope: int = 0           # 1: 3-D rotary position embedding on the self-attention q / k
+    rope_theta: float = 10000.0
+    cond_len: int = 0       # condition tokens of the cross-attention layer (0: no cross-attention)
 
     @property
     def tokens(self) -> int:
@@ -177,12 +183,18 @@ def with_stream(w: Workload, **kw) -> Workload:
 #   W_ada [6C, D_c], b_ada [6C], Wq [C, C], bq [C], Wk [C, C], bk [C],
 #   Wv [C, C], bv [C], Wo [C, C], bo [C], W1 [D_m, C], b1 [D_m],
 #   W2 [C, D_m], b2 [C], gq [d], gk [d]
+# and, for a model with a cross-attention layer (cond_len > 0), then
+#   ln3_w [C], ln3_b [C], Wq_c [C, C], bq_c [C], Wk_c [C, C], bk_c [C],
+#   Wv_c [C, C], bv_c [C], Wo_c [C, C], bo_c [C], gq_c [d], gk_c [d]
 # Blocks are concatenated; the blob is float32.
 # ---------------------------------------------------------------------------
 
+_GAINS = ("gq", "gk", "gq_c", "gk_c")
+
+
 def block_tensor_shapes(m: ModelShape) -> List[Tuple[str, Tuple[int, ...]]]:
     C, Dc, Dm, d = m.hidden, m.cond_dim, m.mlp_hidden, m.head_dim
-    return [
+    shapes = [
         ("w_ada", (6 * C, Dc)), ("b_ada", (6 * C,)),
         ("wq", (C, C)), ("bq", (C,)),
         ("wk", (C, C)), ("bk", (C,)),
@@ -192,6 +204,16 @@ def block_tensor_shapes(m: ModelShape) -> List[Tuple[str, Tuple[int, ...]]]:
         ("w2", (C, Dm)), ("b2", (C,)),
         ("gq", (d,)), ("gk", (d,)),
     ]
+    if m.cond_len > 0:
+        shapes += [
+            ("ln3_w", (C,)), ("ln3_b", (C,)),
+            ("wq_c", (C, C)), ("bq_c", (C,)),
+            ("wk_c", (C, C)), ("bk_c", (C,)),
+            ("wv_c", (C, C)), ("bv_c", (C,)),
+            ("wo_c", (C, C)), ("bo_c", (C,)),
+            ("gq_c", (d,)), ("gk_c", (d,)),
+        ]
+    return shapes
 
 
 def block_numel(m: ModelShape) -> int:
@@ -203,15 +225,18 @@ def weights_numel(m: ModelShape) -> int:
 
 
 def make_weights(m: ModelShape, seed: int = 0, std: float = 0.02) -> np.ndarray:
-    """Flat float32 blob: Linear weights and biases N(0, std^2), gains 1."""
+    """Flat float32 blob: Linear weights and biases N(0, std^2), QK-norm gains 1,
+    cross-attention LayerNorm scale 1 + N(0, std^2) and shift N(0, std^2)."""
     rng = np.random.default_rng(seed)
     out = np.empty(weights_numel(m), dtype=np.float32)
     off = 0
     for _ in range(m.n_blocks):
         for name, shape in block_tensor_shapes(m):
             n = int(np.prod(shape))
-            if name in ("gq", "gk"):
+            if name in _GAINS:
                 out[off:off + n] = 1.0
+            elif name == "ln3_w":
+                out[off:off + n] = (1.0 + rng.standard_normal(n) * std).astype(np.float32)
             else:
                 out[off:off + n] = (rng.standard_normal(n) * std).astype(np.float32)
             off += n
@@ -264,6 +289,14 @@ def action_stream(m: ModelShape, s: StreamParams, seed: int = 0,
             step = s.big_sigma if (s.big_every and n % s.big_every == 0) else s.action_sigma
             a = a + step * z
         yield a.astype(np.float32)
+
+
+def condition_tokens(m: ModelShape, seed: int = 0, n_tokens: int | None = None) -> np.ndarray:
+    """The cross-attention condition: float32 [n_tokens, C] ~ N(0, 1) from
+    ``default_rng(seed + 3)`` (stands in for the text / object / lane embeddings)."""
+    n = m.cond_len if n_tokens is None else n_tokens
+    rng = np.random.default_rng(seed + 3)
+    return rng.standard_normal((n, m.hidden)).astype(np.float32)
 
 
 def timesteps(m: ModelShape) -> List[float]:
