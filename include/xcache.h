@@ -86,7 +86,23 @@ typedef struct xc_view_group {
  * multiples of 128.  Block internals: LayerNorm without affine (eps 1e-6),
  * six-way adaLN modulation from W_ada SiLU(c) + b_ada with
  * c = [sinusoidal temb(timestep); action], QK RMSNorm (eps 1e-6) with gains,
- * softmax attention over the rolling cache (no mask), tanh-GELU MLP. */
+ * softmax attention over the rolling cache (no mask), tanh-GELU MLP.
+ * Optional WAN-style extensions (the paper's model is built on WAN 2.2,
+ * Section 3.1, and injects text / object / lane conditions through
+ * cross-attention, Sections 2.1 and 2.3.2):
+ *   rope = 1: 3-D rotary embedding of the self-attention q and k after their
+ *     RMSNorm (so the cache holds rotated keys): head pairs (2j, 2j+1) rotate
+ *     by p * rope_theta^(-2i/d_a); the first d - 4 floor(d/6) dimensions follow
+ *     the frame position n*F + f (absolute across chunks, n the generation),
+ *     the next 2 floor(d/6) the row h, the last 2 floor(d/6) the column w of
+ *     the token in its camera's grid.  Needs head_dim even and >= 6,
+ *     rope_theta > 1, and every grid dimension < 1024.
+ *   cond_len > 0: a cross-attention layer between the self-attention and the
+ *     MLP: x1 += Wo_c softmax(q_c k_c^T / sqrt(d)) v_c + bo_c with
+ *     q_c = RMSNorm(Wq_c (LN(x1) * ln3_w + ln3_b) + bq_c) * gq_c and
+ *     k_c = RMSNorm(Wk_c cond + bk_c) * gk_c, v_c = Wv_c cond + bv_c over the
+ *     condition tokens set by xc_set_condition (at most cond_len <= 4096).
+ * Fields left zero select the plain block. */
 typedef struct xc_model_config {
   int32_t n_blocks;    /* B                                                */
   int32_t hidden;      /* C                                                */
@@ -100,6 +116,9 @@ typedef struct xc_model_config {
   int32_t kv_window;   /* chunks visible to attention, current included    */
   int32_t n_groups;    /* 1..XC_MAX_GROUPS                                 */
   xc_view_group groups[XC_MAX_GROUPS];
+  int32_t rope;        /* 0: none; 1: 3-D rotary embedding (see above)     */
+  float rope_theta;    /* rotary base (10000 in WAN); ignored if rope == 0 */
+  int32_t cond_len;    /* cross-attention condition capacity; 0: none      */
 } xc_model_config;
 
 /* Gate hyper-parameters; names and defaults follow Table 1. */
@@ -145,9 +164,13 @@ const char* xc_status_string(xc_status s);
  *   weights_host    : host float32 blob, per block in this order, row-major
  *                     [out, in]: W_ada [6C, D_t+A], b_ada [6C], Wq [C, C], bq,
  *                     Wk [C, C], bk, Wv [C, C], bv, Wo [C, C], bo,
- *                     W1 [D_m, C], b1, W2 [C, D_m], b2, gq [d], gk [d];
- *                     blocks concatenated.  Copied (converted to bf16 for
- *                     XC_BF16) before return; the caller may free it.
+ *                     W1 [D_m, C], b1, W2 [C, D_m], b2, gq [d], gk [d],
+ *                     and with cond_len > 0 then ln3_w [C], ln3_b [C],
+ *                     Wq_c [C, C], bq_c, Wk_c [C, C], bk_c, Wv_c [C, C], bv_c,
+ *                     Wo_c [C, C], bo_c, gq_c [d], gk_c [d];
+ *                     blocks concatenated.  Copied (Linear weights converted
+ *                     to bf16 for XC_BF16) before return; the caller may free
+ *                     it.
  *   weights_bytes   : must equal 4 * the blob's element count.
  *   hip_stream      : hipStream_t all work is enqueued on (NULL = default).
  *   out             : receives the handle.
@@ -188,6 +211,22 @@ xc_status xc_forward_chunk(xc_handle* h, int32_t step, float timestep, const flo
 xc_status xc_kv_update(xc_handle* h, float timestep, const float* action_host,
                        const void* x_clean, void* x_out);
 
+/* Condition tokens of the cross-attention layer (models with cond_len > 0;
+ * the text / object / lane embeddings of Sections 2.1 and 2.3.2).
+ *   cond_host : host float32 [n_tokens, C], row-major; copied before return.
+ *   n_tokens  : 1 <= n_tokens <= cond_len.
+ * Computes every block's cross-attention keys and values of these tokens
+ * (bf16 models round the tokens to bf16 first); later passes attend to them
+ * until the next call.  Must be called before the first xc_forward_chunk or
+ * xc_kv_update of such a model (XC_ERR_STATE otherwise) and may be called
+ * again between any two passes; xc_reset keeps it.  The gate does not see
+ * the condition (the paper leaves condition changes to step-0 protection,
+ * the anchor blocks and the cascade through block inputs, Section 2.5).
+ * Errors: XC_ERR_INVALID_ARG (NULL, n_tokens out of range, non-finite
+ * values), XC_ERR_STATE (model has no cross-attention), XC_ERR_HIP.
+ * Synchronises the stream once (the upload). */
+xc_status xc_set_condition(xc_handle* h, const float* cond_host, int32_t n_tokens);
+
 /* Synchronise the stream and copy out counters and per-(t, b) state.
  * Every array pointer may be NULL.  skip_counts: int32 [S * B] (t-major);
  * last_decision: uint8 [B] for the last denoising pass (XC_DEC_*;
@@ -218,11 +257,14 @@ xc_status xc_fingerprint_rows(const xc_model_config* model, const xc_gate_config
  * bracketed by HIP events on the bound stream.  A gated evaluation is two
  * launches: XC_KERN_GATE reads the block input once, forms the fingerprint
  * and compares it with the cached one; XC_KERN_GATE_DECIDE takes the
- * decision. */
+ * decision.  The cross-attention layer's kernels are XC_KERN_CROSS_Q (its
+ * LayerNorm and q projection), XC_KERN_CROSS_ATTENTION and XC_KERN_CROSS_O
+ * (output projection and residual). */
 enum {
   XC_KERN_ATTENTION = 0, XC_KERN_GEMM_QKV = 1, XC_KERN_GEMM_OPROJ = 2, XC_KERN_GEMM_UP = 3,
   XC_KERN_GEMM_DOWN = 4, XC_KERN_GATE = 5, XC_KERN_GATE_DECIDE = 6, XC_KERN_SKIP_ADD = 7, XC_KERN_LN_MOD = 8,
-  XC_KERN_QK_NORM = 9, XC_KERN_ADALN = 10, XC_KERN_COUNT = 11
+  XC_KERN_QK_NORM = 9, XC_KERN_ADALN = 10, XC_KERN_CROSS_Q = 11, XC_KERN_CROSS_ATTENTION = 12,
+  XC_KERN_CROSS_O = 13, XC_KERN_COUNT = 14
 };
 xc_status xc_profile(xc_handle* h, int32_t enable);
 

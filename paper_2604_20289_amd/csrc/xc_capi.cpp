@@ -17,6 +17,12 @@
 //   activations    h, q, o, u in the model dtype, padded to Mpad rows; x1
 //                  and two ping-pong streams (float32 models also stage the
 //                  QKV projection in float32 before the QK-norm kernel).
+//   rotary tables  (rope = 1) per-token packed grid coordinates and the
+//                  (cos, sin) tables; the frame section is rebuilt whenever
+//                  the generation index changes
+//   cross-attention (cond_len > 0) its weights per block, the condition's
+//                  keys K_c [B][H][Lcap_c][D] and V_c^T [B][H][D][Lcap_c],
+//                  the condition tokens in the model dtype [Mcpad][C].
 //
 // One denoising pass enqueues, per block: for a gated block the fingerprint
 // reduction and the decision kernel (its flag stays on the device), then the
@@ -55,6 +61,17 @@ struct xc_handle {
   void* wqkv = nullptr; float* bqkv = nullptr; float* gq = nullptr; float* gk = nullptr;
   void* wo = nullptr; float* bo = nullptr; void* w1 = nullptr; float* b1 = nullptr;
   void* w2 = nullptr; float* b2 = nullptr;
+  // rotary embedding
+  float2* rope_tab = nullptr; int* rope_pos = nullptr; int* rope_slot_frames = nullptr; int* rope_slot_frame = nullptr;
+  RopeArgs rope{};
+  int rope_slots = 0, rope_rows = 0, rope_cols = 0;
+  // cross-attention
+  int Mc = 0, n_cond = 0;
+  long long Mcpad = 0, Lcap_c = 0;
+  void* wqkv_c = nullptr; float* bqkv_c = nullptr; float* gq_c = nullptr; float* gk_c = nullptr;
+  void* wo_c = nullptr; float* bo_c = nullptr; float* ln3_shift = nullptr; float* ln3_scale = nullptr;
+  void* kc_c = nullptr; void* vt_c = nullptr; void* cond_act = nullptr; float* cond_kv = nullptr;
+  float* ones = nullptr;
   // caches
   void* kc = nullptr; void* vt = nullptr; void* rhat = nullptr; float* fp = nullptr;
   float* fp_alt = nullptr;  // second fingerprint set of the refresh-on-compute mode
@@ -129,6 +146,19 @@ xc_status validate_model(const xc_model_config* m) {
     if (m->head_dim != 64 && m->head_dim != 128) return XC_ERR_UNSUPPORTED;
     if (m->hidden % 128 != 0 || m->mlp_hidden % 128 != 0) return XC_ERR_UNSUPPORTED;
   }
+  if (m->rope != 0 && m->rope != 1) return XC_ERR_INVALID_ARG;
+  if (m->rope) {
+    if (m->head_dim % 2 != 0) return XC_ERR_INVALID_ARG;
+    if (!std::isfinite(m->rope_theta) || !(m->rope_theta > 1.f)) return XC_ERR_INVALID_ARG;
+    int slots = 0;
+    for (int i = 0; i < m->n_groups; ++i) {
+      const xc_view_group& g = m->groups[i];
+      if (g.height >= 1024 || g.width >= 1024) return XC_ERR_INVALID_ARG;
+      slots += g.frames;
+      if (slots >= 1024) return XC_ERR_INVALID_ARG;
+    }
+  }
+  if (m->cond_len < 0 || m->cond_len > 4096) return XC_ERR_INVALID_ARG;
   return XC_OK;
 }
 
@@ -327,10 +357,63 @@ P* wptr(void* base, size_t elems_before, size_t esz) {
   return reinterpret_cast<P*>(reinterpret_cast<char*>(base) + elems_before * esz);
 }
 
+// Cross-attention layer of block b on x1 (in place): affine LayerNorm, q
+// projection with the per-head RMSNorm, attention over the condition's keys
+// and values, output projection added without a gate.
+void cross_attention(xc_handle* h, int b, const int* flag) {
+  const int C = h->C, H = h->H, D = h->D;
+  const int L = (int)h->L;
+  const size_t esz = h->esz;
+  const void* wq_c = wptr<void>(h->wqkv_c, (size_t)b * 3 * C * C, esz);
+  {
+    Prof p(h, XC_KERN_CROSS_Q);
+    launch_ln_mod(h->dtype, h->x1, h->ln3_shift + (size_t)b * C, h->ln3_scale + (size_t)b * C, h->hbuf, L, C, flag,
+                  h->st);
+    EpiArgs e{};
+    e.M = L;
+    e.N = C;
+    e.bias = h->bqkv_c + (size_t)b * 3 * C;
+    if (h->dtype == XC_BF16) {
+      e.gq = h->gq_c + (size_t)b * D;
+      e.gk = h->gk_c + (size_t)b * D;
+      e.q_out = h->q;
+      e.H = H;
+      e.D = D;
+      e.Mpad = (int)h->Mpad;
+      e.Lcap = (int)h->Lcap_c;
+      launch_gemm(h->dtype, EPI_QKV, h->hbuf, wq_c, L, C, C, e, flag, h->st);
+    } else {
+      e.out_f32 = h->qkv;
+      launch_gemm(h->dtype, EPI_BIAS_F32, h->hbuf, wq_c, L, C, C, e, flag, h->st);
+      launch_qk_norm(h->dtype, h->qkv, nullptr, nullptr, C, h->gq_c + (size_t)b * D, h->gk_c + (size_t)b * D,
+                     RopeArgs{}, h->q, nullptr, nullptr, L, H, D, (int)h->Mpad, 0, 0, flag, h->st);
+    }
+  }
+  {
+    Prof p(h, XC_KERN_CROSS_ATTENTION);
+    launch_attention(h->dtype, h->q, wptr<void>(h->kc_c, (size_t)b * H * h->Lcap_c * D, esz),
+                     wptr<void>(h->vt_c, (size_t)b * H * h->Lcap_c * D, esz), h->o, h->attn_ws, L, (int)h->Mpad,
+                     (int)h->Lcap_c, h->n_cond, H, D, flag, h->st);
+  }
+  {
+    Prof p(h, XC_KERN_CROSS_O);
+    EpiArgs e{};
+    e.M = L;
+    e.N = C;
+    e.bias = h->bo_c + (size_t)b * C;
+    e.out_f32 = h->x1;
+    e.resid = h->x1;  // each element is read and then written by the same lane
+    e.gate = h->ones;
+    launch_gemm(h->dtype, EPI_OPROJ, h->o, wptr<void>(h->wo_c, (size_t)b * C * C, esz), L, C, C, e, flag, h->st);
+  }
+}
+
 // The compute sequence of block b (Eq. 1, the block of the DiT): LN+modulate,
 // QKV projection, QK-norm and cache write, attention over the visible window,
 // output projection with gated residual, LN+modulate, MLP up with GELU, MLP
-// down with gated residual and (for gated blocks) the cached-residual store.
+// down with gated residual and (for gated blocks) the cached-residual store;
+// models with a cross-attention layer run it between the output projection
+// and the second LN+modulate.
 // kv_only: stop after the key/value cache write (the block's output is not
 // needed: the last block of a KV-update pass whose caller takes no output).
 void compute_block(xc_handle* h, int b, const float* x, float* out, const int* flag, void* rhat_tb,
@@ -364,6 +447,7 @@ void compute_block(xc_handle* h, int b, const float* x, float* out, const int* f
     e.Mpad = (int)h->Mpad;
     e.Lcap = (int)h->Lcap;
     e.kv_off = (int)kv_off;
+    e.rope = h->rope;
     launch_gemm(h->dtype, EPI_QKV, h->hbuf, wptr<void>(h->wqkv, (size_t)b * 3 * C * C, esz), L, 3 * C, C, e, flag,
                 h->st);
   } else {
@@ -378,8 +462,9 @@ void compute_block(xc_handle* h, int b, const float* x, float* out, const int* f
                   flag, h->st);
     }
     Prof p(h, XC_KERN_QK_NORM);
-    launch_qk_norm(h->dtype, h->qkv, h->gq + (size_t)b * D, h->gk + (size_t)b * D, h->q, kc_b, vt_b, L, H, D,
-                   (int)h->Mpad, (int)h->Lcap, (int)kv_off, flag, h->st);
+    launch_qk_norm(h->dtype, h->qkv, h->qkv + C, h->qkv + 2 * C, 3 * C, h->gq + (size_t)b * D,
+                   h->gk + (size_t)b * D, h->rope, h->q, kc_b, vt_b, L, H, D, (int)h->Mpad, (int)h->Lcap,
+                   (int)kv_off, flag, h->st);
   }
   if (kv_only) return;
   {
@@ -398,6 +483,7 @@ void compute_block(xc_handle* h, int b, const float* x, float* out, const int* f
     e.gate = gate1;
     launch_gemm(h->dtype, EPI_OPROJ, h->o, wptr<void>(h->wo, (size_t)b * C * C, esz), L, C, C, e, flag, h->st);
   }
+  if (h->Mc > 0) cross_attention(h, b, flag);
   {
     Prof p(h, XC_KERN_LN_MOD);
     launch_ln_mod(h->dtype, h->x1, shift2, scale2, h->hbuf, L, C, flag, h->st);
@@ -482,6 +568,56 @@ void build_tables(xc_handle* h) {
 
 }
 
+// Rotary embedding: per-token packed (frame slot, h, w) and the table layout
+// (frame slots, then rows 0..H_max-1, then columns 0..W_max-1).
+void build_rope(xc_handle* h) {
+  const xc_model_config* m = &h->m;
+  std::vector<int> pos, slot_frames, slot_frame;
+  int slot0 = 0, rows = 1, cols = 1;
+  for (int gi = 0; gi < m->n_groups; ++gi) {
+    const xc_view_group& vg = m->groups[gi];
+    for (int v = 0; v < vg.views; ++v)
+      for (int f = 0; f < vg.frames; ++f)
+        for (int y = 0; y < vg.height; ++y)
+          for (int x = 0; x < vg.width; ++x) pos.push_back((slot0 + f) | (y << 10) | (x << 20));
+    for (int f = 0; f < vg.frames; ++f) {
+      slot_frames.push_back(vg.frames);
+      slot_frame.push_back(f);
+    }
+    slot0 += vg.frames;
+    rows = std::max(rows, vg.height);
+    cols = std::max(cols, vg.width);
+  }
+  const int s6 = h->D / 6;
+  RopeArgs& r = h->rope;
+  r.np[0] = (h->D - 4 * s6) / 2;
+  r.np[1] = s6;
+  r.np[2] = s6;
+  r.off[0] = 0;
+  r.off[1] = slot0 * r.np[0];
+  r.off[2] = r.off[1] + rows * r.np[1];
+  const int entries = r.off[2] + cols * r.np[2];
+  h->rope_slots = slot0;
+  h->rope_rows = rows;
+  h->rope_cols = cols;
+  h->rope_tab = dalloc_t<float2>(h, entries);
+  h->rope_pos = dalloc_t<int>(h, pos.size());
+  h->rope_slot_frames = dalloc_t<int>(h, slot_frames.size());
+  h->rope_slot_frame = dalloc_t<int>(h, slot_frame.size());
+  XC_HIP(hipMemcpy(h->rope_pos, pos.data(), pos.size() * 4, hipMemcpyHostToDevice));
+  XC_HIP(hipMemcpy(h->rope_slot_frames, slot_frames.data(), slot_frames.size() * 4, hipMemcpyHostToDevice));
+  XC_HIP(hipMemcpy(h->rope_slot_frame, slot_frame.data(), slot_frame.size() * 4, hipMemcpyHostToDevice));
+  r.tab = h->rope_tab;
+  r.pos = h->rope_pos;
+}
+
+// Frame positions follow the generation index: refill the tables for h->n.
+void refresh_rope(xc_handle* h) {
+  if (h->rope.tab == nullptr) return;
+  launch_rope_table(h->rope_tab, h->rope, h->rope_slots, h->rope_slot_frames, h->rope_slot_frame, h->rope_rows,
+                    h->rope_cols, (double)h->m.rope_theta, h->n, h->st);
+}
+
 void reset_state(xc_handle* h) {
   const size_t SB = (size_t)h->S * h->B;
   XC_HIP(hipMemsetAsync(h->kc, 0, (size_t)h->B * h->H * h->Lcap * h->D * h->esz, h->st));
@@ -498,8 +634,10 @@ void reset_state(xc_handle* h) {
   launch_fill_f32(h->rec_d, __builtin_nanf(""), h->B, h->st);
   launch_fill_f32(h->rec_tau, __builtin_nanf(""), h->B, h->st);
   if (check_launch() != XC_OK) throw Fail{XC_ERR_HIP};
-  XC_HIP(hipStreamSynchronize(h->st));
   h->n = 0;
+  refresh_rope(h);
+  if (check_launch() != XC_OK) throw Fail{XC_ERR_HIP};
+  XC_HIP(hipStreamSynchronize(h->st));
   h->visited.assign(SB, 0);
   h->evals_post_warmup = h->gated_evals = h->kv_block_evals = 0;
   h->last_step = -1;
@@ -536,6 +674,16 @@ void init_device(xc_handle* h, const float* w) {
   h->b1 = dalloc_t<float>(h, (size_t)B * Dm);
   h->w2 = dalloc(h, (size_t)B * C * Dm * esz);
   h->b2 = dalloc_t<float>(h, (size_t)B * C);
+  if (h->Mc > 0) {
+    h->ln3_scale = dalloc_t<float>(h, (size_t)B * C);
+    h->ln3_shift = dalloc_t<float>(h, (size_t)B * C);
+    h->wqkv_c = dalloc(h, (size_t)B * 3 * C * C * esz);
+    h->bqkv_c = dalloc_t<float>(h, (size_t)B * 3 * C);
+    h->wo_c = dalloc(h, (size_t)B * C * C * esz);
+    h->bo_c = dalloc_t<float>(h, (size_t)B * C);
+    h->gq_c = dalloc_t<float>(h, (size_t)B * D);
+    h->gk_c = dalloc_t<float>(h, (size_t)B * D);
+  }
 
   // upload, block by block, in the blob order
   std::vector<uint16_t> stage;
@@ -568,6 +716,29 @@ void init_device(xc_handle* h, const float* w) {
     off += D;
     upload(h, w + off, D, h->gk + (size_t)b * D, false, stage);
     off += D;
+    if (h->Mc > 0) {
+      // LayerNorm scale w enters the modulated-LN kernel as 1 + (w - 1)
+      std::vector<float> sc(w + off, w + off + C);
+      for (float& v : sc) v -= 1.0f;
+      upload(h, sc.data(), C, h->ln3_scale + (size_t)b * C, false, stage);
+      off += C;
+      upload(h, w + off, C, h->ln3_shift + (size_t)b * C, false, stage);
+      off += C;
+      for (int part = 0; part < 3; ++part) {  // Wq_c, bq_c, Wk_c, bk_c, Wv_c, bv_c
+        upload(h, w + off, CC, wptr<void>(h->wqkv_c, (size_t)b * 3 * CC + part * CC, esz), bf, stage);
+        off += CC;
+        upload(h, w + off, C, h->bqkv_c + (size_t)b * 3 * C + part * C, false, stage);
+        off += C;
+      }
+      upload(h, w + off, CC, wptr<void>(h->wo_c, (size_t)b * CC, esz), bf, stage);
+      off += CC;
+      upload(h, w + off, C, h->bo_c + (size_t)b * C, false, stage);
+      off += C;
+      upload(h, w + off, D, h->gq_c + (size_t)b * D, false, stage);
+      off += D;
+      upload(h, w + off, D, h->gk_c + (size_t)b * D, false, stage);
+      off += D;
+    }
   }
 
   h->kc = dalloc(h, (size_t)B * H * h->Lcap * D * esz);
@@ -596,8 +767,22 @@ void init_device(xc_handle* h, const float* w) {
   if (bf) {
     size_t ws = 0;  // the key window grows chunk by chunk: size for the largest need
     for (int w = 1; w <= h->Wkv; ++w) ws = std::max(ws, attention_workspace_floats((int)h->L, (int)(w * h->L), H, D));
+    for (int n = 1; n <= h->Mc; ++n) ws = std::max(ws, attention_workspace_floats((int)h->L, n, H, D));
     if (ws) h->attn_ws = dalloc_t<float>(h, ws);
   }
+  if (h->Mc > 0) {
+    h->kc_c = dalloc(h, (size_t)B * H * h->Lcap_c * D * esz);
+    h->vt_c = dalloc(h, (size_t)B * H * h->Lcap_c * D * esz);
+    h->cond_act = dalloc(h, (size_t)h->Mcpad * C * esz);
+    if (!bf) h->cond_kv = dalloc_t<float>(h, (size_t)h->Mcpad * 2 * C);
+    h->ones = dalloc_t<float>(h, C);
+    launch_fill_f32(h->ones, 1.0f, C, h->st);
+    // keys past the valid condition tokens and padded token rows must be finite
+    XC_HIP(hipMemsetAsync(h->kc_c, 0, (size_t)B * H * h->Lcap_c * D * esz, h->st));
+    XC_HIP(hipMemsetAsync(h->vt_c, 0, (size_t)B * H * h->Lcap_c * D * esz, h->st));
+    XC_HIP(hipMemsetAsync(h->cond_act, 0, (size_t)h->Mcpad * C * esz, h->st));
+  }
+  if (h->m.rope) build_rope(h);
   // padded activation rows are read by the tile loads and must be finite
   XC_HIP(hipMemsetAsync(h->hbuf, 0, (size_t)h->Mpad * C * esz, h->st));
   XC_HIP(hipMemsetAsync(h->q, 0, (size_t)H * h->Mpad * D * esz, h->st));
@@ -658,7 +843,8 @@ xc_status xc_init(const xc_model_config* model, const xc_gate_config* gate, cons
   s = validate_gate(gate, model);
   if (s != XC_OK) return s;
   const long long C = model->hidden, Dc = model->temb_dim + model->action_dim, Dm = model->mlp_hidden;
-  const long long per_block = 6 * C * Dc + 6 * C + 4 * (C * C + C) + 2 * Dm * C + Dm + C + 2 * model->head_dim;
+  const long long per_block = 6 * C * Dc + 6 * C + 4 * (C * C + C) + 2 * Dm * C + Dm + C + 2 * model->head_dim +
+                              (model->cond_len > 0 ? 2 * C + 4 * (C * C + C) + 2 * model->head_dim : 0);
   if (weights_bytes != (size_t)(per_block * model->n_blocks) * sizeof(float)) return XC_ERR_INVALID_ARG;
 
   xc_handle* h = new (std::nothrow) xc_handle();
@@ -683,6 +869,9 @@ xc_status xc_init(const xc_model_config* model, const xc_gate_config* gate, cons
   // 256-query attention tiles: roundup(L, 256) + 256 >= roundup(L, 192)
   h->Mpad = (h->L + 255) / 256 * 256 + 256;
   h->Lcap = ((long long)h->Wkv * h->L + 63) / 64 * 64;
+  h->Mc = model->cond_len;
+  h->Mcpad = ((long long)h->Mc + 255) / 256 * 256 + 256;
+  h->Lcap_c = ((long long)h->Mc + 63) / 64 * 64;
   try {
     XC_HIP(hipGetDevice(&h->device));
     init_device(h, weights_host);
@@ -704,6 +893,7 @@ xc_status xc_forward_chunk(xc_handle* h, int32_t step, float timestep, const flo
                            void* x_out, uint32_t flags) {
   if (!h || !action_host || !x_in || !x_out) return XC_ERR_INVALID_ARG;
   if (h->sticky) return XC_ERR_HIP;
+  if (h->Mc > 0 && h->n_cond == 0) return XC_ERR_STATE;
   if (step < 0 || step >= h->S) return XC_ERR_INVALID_ARG;
   if ((flags & ~(uint32_t)XC_FORCE_FULL) != 0) return XC_ERR_INVALID_ARG;
   if (!std::isfinite(timestep)) return XC_ERR_INVALID_ARG;
@@ -764,6 +954,7 @@ xc_status xc_forward_chunk(xc_handle* h, int32_t step, float timestep, const flo
 xc_status xc_kv_update(xc_handle* h, float timestep, const float* action_host, const void* x_clean, void* x_out) {
   if (!h || !action_host || !x_clean) return XC_ERR_INVALID_ARG;
   if (h->sticky) return XC_ERR_HIP;
+  if (h->Mc > 0 && h->n_cond == 0) return XC_ERR_STATE;
   if (!std::isfinite(timestep)) return XC_ERR_INVALID_ARG;
   for (int i = 0; i < h->A; ++i)
     if (!std::isfinite(action_host[i])) return XC_ERR_INVALID_ARG;
@@ -783,10 +974,64 @@ xc_status xc_kv_update(xc_handle* h, float timestep, const float* action_host, c
     for (int i = 0; i < h->A; ++i) h->action_prev[i] = action_host[i];
     h->have_action_prev = true;
     h->n += 1;
+    refresh_rope(h);
     h->last_step = h->S;
     if (check_launch() != XC_OK) throw Fail{XC_ERR_HIP};
   } catch (const Fail& f) {
     if (f.s == XC_ERR_HIP) h->sticky = true;
+    return f.s;
+  }
+  return XC_OK;
+}
+
+xc_status xc_set_condition(xc_handle* h, const float* cond_host, int32_t n_tokens) {
+  if (!h || !cond_host) return XC_ERR_INVALID_ARG;
+  if (h->sticky) return XC_ERR_HIP;
+  if (h->Mc == 0) return XC_ERR_STATE;
+  if (n_tokens < 1 || n_tokens > h->Mc) return XC_ERR_INVALID_ARG;
+  const int C = h->C, H = h->H, D = h->D;
+  const size_t count = (size_t)n_tokens * C;
+  for (size_t i = 0; i < count; ++i)
+    if (!std::isfinite(cond_host[i])) return XC_ERR_INVALID_ARG;
+  try {
+    XC_HIP(hipSetDevice(h->device));
+    const bool bf = h->dtype == XC_BF16;
+    const size_t esz = h->esz;
+    std::vector<uint16_t> stage;
+    upload(h, cond_host, count, h->cond_act, bf, stage);
+    // each block's K_c = RMSNorm(Wk_c cond + bk_c) * gk_c and V_c = Wv_c cond + bv_c
+    for (int b = 0; b < h->B; ++b) {
+      const void* wkv = wptr<void>(h->wqkv_c, (size_t)b * 3 * C * C + (size_t)C * C, esz);
+      void* kc_b = wptr<void>(h->kc_c, (size_t)b * H * h->Lcap_c * D, esz);
+      void* vt_b = wptr<void>(h->vt_c, (size_t)b * H * h->Lcap_c * D, esz);
+      EpiArgs e{};
+      e.M = n_tokens;
+      e.N = 2 * C;
+      e.bias = h->bqkv_c + (size_t)b * 3 * C + C;
+      if (bf) {
+        e.part_base = 1;
+        e.gq = h->gq_c + (size_t)b * D;
+        e.gk = h->gk_c + (size_t)b * D;
+        e.k_cache = kc_b;
+        e.vt_cache = vt_b;
+        e.H = H;
+        e.D = D;
+        e.Mpad = (int)h->Mcpad;
+        e.Lcap = (int)h->Lcap_c;
+        launch_gemm(h->dtype, EPI_QKV, h->cond_act, wkv, n_tokens, 2 * C, C, e, nullptr, h->st);
+      } else {
+        e.out_f32 = h->cond_kv;
+        launch_gemm(h->dtype, EPI_BIAS_F32, h->cond_act, wkv, n_tokens, 2 * C, C, e, nullptr, h->st);
+        launch_qk_norm(h->dtype, nullptr, h->cond_kv, h->cond_kv + C, 2 * C, h->gq_c + (size_t)b * D,
+                       h->gk_c + (size_t)b * D, RopeArgs{}, nullptr, kc_b, vt_b, n_tokens, H, D, 0,
+                       (int)h->Lcap_c, 0, nullptr, h->st);
+      }
+    }
+    if (check_launch() != XC_OK) throw Fail{XC_ERR_HIP};
+    XC_HIP(hipStreamSynchronize(h->st));
+    h->n_cond = n_tokens;
+  } catch (const Fail& f) {
+    h->sticky = true;
     return f.s;
   }
   return XC_OK;

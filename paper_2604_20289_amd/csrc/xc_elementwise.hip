@@ -176,45 +176,95 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const float* __restrict__ x
 //   v                       -> V^T cache [H][D][Lcap] at column kv_off + m
 // The V tile is transposed through LDS so the V^T rows are written coalesced.
 template <typename T>
-__global__ __launch_bounds__(256) void qk_norm_kernel(const float* __restrict__ qkv, const float* __restrict__ gq,
-                                                      const float* __restrict__ gk, T* __restrict__ q,
-                                                      T* __restrict__ kring, T* __restrict__ vtring, int L, int H,
-                                                      int D, int Mpad, int Lcap, int kv_off,
-                                                      const int* __restrict__ flag) {
+__global__ __launch_bounds__(256) void qk_norm_kernel(const float* __restrict__ qs, const float* __restrict__ ks,
+                                                      const float* __restrict__ vs, int ld,
+                                                      const float* __restrict__ gq, const float* __restrict__ gk,
+                                                      RopeArgs rope, T* __restrict__ q, T* __restrict__ kring,
+                                                      T* __restrict__ vtring, int L, int H, int D, int Mpad,
+                                                      int Lcap, int kv_off, const int* __restrict__ flag) {
   if (flag != nullptr && *flag) return;
   __shared__ float s_v[64][129];
   const int tile = blockIdx.x, h = blockIdx.y;
-  const int C = H * D;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int m0 = tile * 64;
-  // q and k: each wave takes 16 tokens
+  // q and k: each wave takes 16 tokens; lane holds head dims lane, lane + 64
   for (int i = 0; i < 16; ++i) {
     int tl = wave * 16 + i;
     int m = m0 + tl;
     if (m >= L) break;
-    const float* row = qkv + (long long)m * 3 * C + h * D;
 #pragma unroll
     for (int part = 0; part < 2; ++part) {
-      const float* src = row + part * C;
+      const float* base = part == 0 ? qs : ks;
+      if (base == nullptr) continue;
+      const float* src = base + (long long)m * ld + h * D;
       const float* g = part == 0 ? gq : gk;
       float a0 = lane < D ? src[lane] : 0.f;
       float a1 = lane + 64 < D ? src[lane + 64] : 0.f;
       float ss = wave_sum(a0 * a0 + a1 * a1);
       float r = 1.0f / sqrtf(ss / (float)D + 1e-6f);
+      a0 = lane < D ? a0 * r * g[lane] : 0.f;
+      a1 = lane + 64 < D ? a1 * r * g[lane + 64] : 0.f;
+      if (rope.tab != nullptr) {
+        // pair (2j, 2j+1) sits in lanes (2j, 2j+1): (a, b) -> (a c - b s, a s + b c)
+        const float p0 = __shfl_xor(a0, 1, 64), p1 = __shfl_xor(a1, 1, 64);
+        const float sgn = (lane & 1) ? 1.f : -1.f;
+        if (lane < D) {
+          const float2 cs = rope_cs(rope, m, lane >> 1);
+          a0 = a0 * cs.x + sgn * p0 * cs.y;
+        }
+        if (lane + 64 < D) {
+          const float2 cs = rope_cs(rope, m, (lane + 64) >> 1);
+          a1 = a1 * cs.x + sgn * p1 * cs.y;
+        }
+      }
       T* dst = part == 0 ? q + ((long long)h * Mpad + m) * D : kring + ((long long)h * Lcap + kv_off + m) * D;
-      if (lane < D) dst[lane] = to_t<T>(a0 * r * g[lane]);
-      if (lane + 64 < D) dst[lane + 64] = to_t<T>(a1 * r * g[lane + 64]);
+      if (lane < D) dst[lane] = to_t<T>(a0);
+      if (lane + 64 < D) dst[lane + 64] = to_t<T>(a1);
     }
-    const float* vsrc = row + 2 * C;
-    if (lane < D) s_v[tl][lane] = vsrc[lane];
-    if (lane + 64 < D) s_v[tl][lane + 64] = vsrc[lane + 64];
+    if (vs != nullptr) {
+      const float* vsrc = vs + (long long)m * ld + h * D;
+      if (lane < D) s_v[tl][lane] = vsrc[lane];
+      if (lane + 64 < D) s_v[tl][lane + 64] = vsrc[lane + 64];
+    }
   }
+  if (vs == nullptr) return;
   __syncthreads();
   // V^T: row dd holds 64 consecutive tokens
   const int nt = min(64, L - m0);
   for (int idx = threadIdx.x; idx < D * 64; idx += 256) {
     int dd = idx >> 6, tl = idx & 63;
     if (tl < nt) vtring[((long long)h * D + dd) * Lcap + kv_off + m0 + tl] = to_t<T>(s_v[tl][dd]);
+  }
+}
+
+// Rotary tables (see RopeArgs): entry idx of the contiguous frame / row /
+// column sections gets (cos, sin) of position * theta^(-2i/d_a), evaluated in
+// double (frame positions grow with the generation index).
+__global__ void rope_table_kernel(float2* __restrict__ tab, RopeArgs r, int n_slots,
+                                  const int* __restrict__ slot_frames, const int* __restrict__ slot_frame, int rows,
+                                  int cols, double log_theta, long long n) {
+  const int n0 = n_slots * r.np[0], n1 = rows * r.np[1], n2 = cols * r.np[2];
+  for (int idx = blockIdx.x * blockDim.x + threadIdx.x; idx < n0 + n1 + n2; idx += gridDim.x * blockDim.x) {
+    double pos;
+    int i, np;
+    if (idx < n0) {
+      const int s = idx / r.np[0];
+      i = idx - s * r.np[0];
+      np = r.np[0];
+      pos = (double)n * slot_frames[s] + slot_frame[s];
+    } else if (idx < n0 + n1) {
+      const int k = idx - n0, p = k / r.np[1];
+      i = k - p * r.np[1];
+      np = r.np[1];
+      pos = p;
+    } else {
+      const int k = idx - n0 - n1, p = k / r.np[2];
+      i = k - p * r.np[2];
+      np = r.np[2];
+      pos = p;
+    }
+    const double ang = pos * exp(-2.0 * i / (2.0 * np) * log_theta);
+    tab[idx] = make_float2((float)cos(ang), (float)sin(ang));
   }
 }
 
@@ -303,16 +353,23 @@ void launch_ln_mod(int dtype, const float* x, const float* shift, const float* s
 #undef XC_LN
 }
 
-void launch_qk_norm(int dtype, const float* qkv, const float* gq, const float* gk, void* q, void* kring,
-                    void* vtring, int L, int H, int D, int Mpad, int Lcap, int kv_off, const int* flag,
-                    hipStream_t st) {
+void launch_qk_norm(int dtype, const float* qs, const float* ks, const float* vs, int ld, const float* gq,
+                    const float* gk, const RopeArgs& rope, void* q, void* kring, void* vtring, int L, int H, int D,
+                    int Mpad, int Lcap, int kv_off, const int* flag, hipStream_t st) {
   dim3 grid((L + 63) / 64, H);
   if (dtype == 1)
-    qk_norm_kernel<bf16><<<grid, 256, 0, st>>>(qkv, gq, gk, (bf16*)q, (bf16*)kring, (bf16*)vtring, L, H, D, Mpad,
-                                               Lcap, kv_off, flag);
+    qk_norm_kernel<bf16><<<grid, 256, 0, st>>>(qs, ks, vs, ld, gq, gk, rope, (bf16*)q, (bf16*)kring,
+                                               (bf16*)vtring, L, H, D, Mpad, Lcap, kv_off, flag);
   else
-    qk_norm_kernel<float><<<grid, 256, 0, st>>>(qkv, gq, gk, (float*)q, (float*)kring, (float*)vtring, L, H, D,
-                                                Mpad, Lcap, kv_off, flag);
+    qk_norm_kernel<float><<<grid, 256, 0, st>>>(qs, ks, vs, ld, gq, gk, rope, (float*)q, (float*)kring,
+                                                (float*)vtring, L, H, D, Mpad, Lcap, kv_off, flag);
+}
+
+void launch_rope_table(float2* tab, const RopeArgs& r, int n_slots, const int* slot_frames, const int* slot_frame,
+                       int rows, int cols, double theta, long long n, hipStream_t st) {
+  const int total = n_slots * r.np[0] + rows * r.np[1] + cols * r.np[2];
+  rope_table_kernel<<<(total + 255) / 256, 256, 0, st>>>(tab, r, n_slots, slot_frames, slot_frame, rows, cols,
+                                                         log(theta), n);
 }
 
 void launch_skip_add(int dtype, const float* x, const void* rhat, float* out, long long n, const int* flag,

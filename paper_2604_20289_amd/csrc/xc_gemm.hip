@@ -205,8 +205,9 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(const bf16* __restric
   // tile column wn*NT*32 + nt*32 + lo
   if constexpr (MODE == EPI_QKV) {
     const int C = e.H * e.D;
-    const int part = n0 / C;  // 0 q, 1 k, 2 v (a tile never straddles two parts)
-    const int head0 = (n0 - part * C) / e.D;
+    const int lpart = n0 / C;            // a tile never straddles two column blocks
+    const int part = lpart + e.part_base;  // 0 q, 1 k, 2 v
+    const int head0 = (n0 - lpart * C) / e.D;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -241,6 +242,7 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(const bf16* __restric
       }
       __syncthreads();
       const float* gain = part == 0 ? e.gq : e.gk;
+      const bool rope = e.rope.tab != nullptr;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -249,12 +251,19 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(const bf16* __restric
           for (int r = 0; r < 4; ++r) {
             const int trow = wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r;
             const int row = m0 + trow;
-            if (row >= M) continue;
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) {
               const int tcol = wn * NT * 32 + nt * 32 + lo;
               const int hd = tcol / e.D, dd = tcol - hd * e.D;
-              const float v = acc[mt][nt][g * 4 + r] * ss[trow * 65 + 64 - hd] * gain[dd];
+              float v = acc[mt][nt][g * 4 + r] * ss[trow * 65 + 64 - hd] * gain[dd];
+              if (rope) {
+                // rotary pair (dd & ~1, dd | 1) = lanes (lo & ~1, lo | 1) of the same row:
+                // (a, b) -> (a c - b s, a s + b c); rows past M use a clamped table row
+                const float pv = __shfl_xor(v, 1, 64);
+                const float2 cs = rope_cs(e.rope, min(row, M - 1), dd >> 1);
+                v = v * cs.x + ((lo & 1) ? pv : -pv) * cs.y;
+              }
+              if (row >= M) continue;
               const long long hh = head0 + hd;
               bf16* dst = part == 0 ? reinterpret_cast<bf16*>(e.q_out) + (hh * e.Mpad + row) * e.D + dd
                                     : reinterpret_cast<bf16*>(e.k_cache) + (hh * e.Lcap + e.kv_off + row) * e.D + dd;

@@ -28,6 +28,28 @@ enum EpiMode : int {
   EPI_QKV = 4,       // acc + bias; per-head RMSNorm * gain on q and k; q -> q_out, k/v -> caches (bf16)
 };
 
+// 3-D rotary embedding tables (device).  Pair i of axis a (0 frame, 1 row,
+// 2 column) at axis position p is tab[off[a] + p * np[a] + i] = (cos, sin) of
+// the rotation angle.  The frame section is indexed by frame slot (one slot
+// per (view group, frame) pair) and rebuilt for each generation; pos[row]
+// packs the row's frame slot | h << 10 | w << 20.  tab == null: no rotation.
+struct RopeArgs {
+  const float2* tab;
+  const int* pos;
+  int np[3];
+  int off[3];
+};
+
+// (cos, sin) of head pair `pair` for token `row`.
+__device__ __forceinline__ float2 rope_cs(const RopeArgs& r, int row, int pair) {
+  const int packed = r.pos[row];
+  if (pair < r.np[0]) return r.tab[r.off[0] + (packed & 1023) * r.np[0] + pair];
+  pair -= r.np[0];
+  if (pair < r.np[1]) return r.tab[r.off[1] + ((packed >> 10) & 1023) * r.np[1] + pair];
+  pair -= r.np[1];
+  return r.tab[r.off[2] + ((packed >> 20) & 1023) * r.np[2] + pair];
+}
+
 struct EpiArgs {
   int M;               // valid rows
   int N;               // columns (row stride of every output)
@@ -37,7 +59,10 @@ struct EpiArgs {
   const float* resid;  // [M][N]
   const float* gate;   // [N]
   const float* xin;    // [M][N]
-  // EPI_QKV: columns [0, C) are q, [C, 2C) k, [2C, 3C) v, C = H * D
+  // EPI_QKV: column block j (C = H * D columns each) is part part_base + j
+  // of (q, k, v): part_base 0 for the [q; k; v] projection, 1 for [k; v]
+  int part_base;
+  RopeArgs rope;       // rotation of q and k (tab == null: none)
   const float* gq;     // [D]
   const float* gk;     // [D]
   void* q_out;         // [H][Mpad][D]
@@ -94,9 +119,20 @@ void launch_ln_mod(int dtype, const float* x, const float* shift, const float* s
                    const int* flag, hipStream_t st);
 void launch_gemm(int dtype, EpiMode mode, const void* A, const void* W, int M, int N, int K, const EpiArgs& e,
                  const int* flag, hipStream_t st);
-void launch_qk_norm(int dtype, const float* qkv, const float* gq, const float* gk, void* q, void* kring,
-                    void* vtring, int L, int H, int D, int Mpad, int Lcap, int kv_off, const int* flag,
-                    hipStream_t st);
+// float32 models: per-head RMSNorm * gain of q and k (with the rotary
+// embedding when rope.tab != null), q -> q [H][Mpad][D], k / v -> the caches
+// at row / column kv_off + m.  qs, ks, vs: column 0 of each part in a
+// row-major [L][ld] float32 matrix; a null part is skipped.
+void launch_qk_norm(int dtype, const float* qs, const float* ks, const float* vs, int ld, const float* gq,
+                    const float* gk, const RopeArgs& rope, void* q, void* kring, void* vtring, int L, int H, int D,
+                    int Mpad, int Lcap, int kv_off, const int* flag, hipStream_t st);
+// Rebuilds the rotary tables for generation n: frame slot s has position
+// n * slot_frames[s] + slot_frame[s]; row and column sections hold positions
+// 0 .. rows-1 and 0 .. cols-1, the three sections contiguous in that order
+// (r.off = {0, n_slots * np[0], n_slots * np[0] + rows * np[1]}); theta: rotary
+// base.
+void launch_rope_table(float2* tab, const RopeArgs& r, int n_slots, const int* slot_frames, const int* slot_frame,
+                       int rows, int cols, double theta, long long n, hipStream_t st);
 // Floats of the attention workspace (partials of items whose keys are split
 // across workgroups) for L queries over Lk keys, H heads of dimension D.
 size_t attention_workspace_floats(int L, int Lk, int H, int D);

@@ -28,13 +28,13 @@ XC_DEC_COMPUTE, XC_DEC_SKIP, XC_DEC_FORCED, XC_DEC_NONE = 0, 1, 2, 255
 XC_MAX_GROUPS = 8
 (XC_KERN_ATTENTION, XC_KERN_GEMM_QKV, XC_KERN_GEMM_OPROJ, XC_KERN_GEMM_UP, XC_KERN_GEMM_DOWN,
  XC_KERN_GATE, XC_KERN_GATE_DECIDE, XC_KERN_SKIP_ADD, XC_KERN_LN_MOD, XC_KERN_QK_NORM, XC_KERN_ADALN,
- XC_KERN_COUNT) = range(12)
+ XC_KERN_CROSS_Q, XC_KERN_CROSS_ATTENTION, XC_KERN_CROSS_O, XC_KERN_COUNT) = range(15)
 
 KERNEL_NAMES = ["attention", "gemm_qkv", "gemm_oproj", "gemm_up", "gemm_down", "gate", "gate_decide", "skip_add",
-                "ln_mod", "qk_norm", "adaln"]
+                "ln_mod", "qk_norm", "adaln", "cross_q", "cross_attention", "cross_o"]
 
-EXPORTED = ["xc_status_string", "xc_init", "xc_forward_chunk", "xc_kv_update", "xc_stats", "xc_reset",
-            "xc_destroy", "xc_axpby", "xc_fingerprint_rows", "xc_profile", "xc_kernel_times"]
+EXPORTED = ["xc_status_string", "xc_init", "xc_forward_chunk", "xc_kv_update", "xc_set_condition", "xc_stats",
+            "xc_reset", "xc_destroy", "xc_axpby", "xc_fingerprint_rows", "xc_profile", "xc_kernel_times"]
 
 
 class ViewGroupC(ctypes.Structure):
@@ -47,7 +47,8 @@ class ModelConfigC(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("mlp_hidden", ctypes.c_int32), ("temb_dim", ctypes.c_int32),
                 ("action_dim", ctypes.c_int32), ("dtype", ctypes.c_int32), ("n_steps", ctypes.c_int32),
                 ("kv_window", ctypes.c_int32), ("n_groups", ctypes.c_int32),
-                ("groups", ViewGroupC * XC_MAX_GROUPS)]
+                ("groups", ViewGroupC * XC_MAX_GROUPS), ("rope", ctypes.c_int32), ("rope_theta", ctypes.c_float),
+                ("cond_len", ctypes.c_int32)]
 
 
 class GateConfigC(ctypes.Structure):
@@ -92,6 +93,7 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
         "xc_init": (i32, [P(ModelConfigC), P(GateConfigC), vp, sz, vp, P(vp)]),
         "xc_forward_chunk": (i32, [vp, i32, f32, vp, vp, vp, u32]),
         "xc_kv_update": (i32, [vp, f32, vp, vp, vp]),
+        "xc_set_condition": (i32, [vp, vp, i32]),
         "xc_stats": (i32, [vp, P(StatsC), vp, vp, vp, vp, vp, vp]),
         "xc_reset": (i32, [vp]),
         "xc_destroy": (i32, [vp]),
@@ -133,6 +135,9 @@ def model_config(model) -> ModelConfigC:
     c.n_groups = len(groups)
     for i, g in enumerate(groups[:XC_MAX_GROUPS]):
         c.groups[i] = ViewGroupC(g.views, g.frames, g.height, g.width)
+    c.rope = getattr(model, "rope", 0)
+    c.rope_theta = getattr(model, "rope_theta", 10000.0)
+    c.cond_len = getattr(model, "cond_len", 0)
     return c
 
 
@@ -175,6 +180,13 @@ def xc_forward_chunk(h: int, step: int, timestep: float, action: np.ndarray, x_i
 def xc_kv_update(h: int, timestep: float, action: np.ndarray, x_clean, x_out=None):
     a = np.ascontiguousarray(action, dtype=np.float32)
     _check(load_library().xc_kv_update(h, timestep, a.ctypes.data, _ptr(x_clean), _ptr(x_out)), "xc_kv_update")
+
+
+def xc_set_condition(h: int, cond: np.ndarray):
+    c = np.ascontiguousarray(cond, dtype=np.float32)
+    if c.ndim != 2:
+        raise ValueError("condition tokens must be [n_tokens, hidden]")
+    _check(load_library().xc_set_condition(h, c.ctypes.data, c.shape[0]), "xc_set_condition")
 
 
 def xc_stats(h: int, n_steps: int, n_blocks: int) -> dict:
@@ -244,6 +256,9 @@ class XCache:
 
     def forward_chunk(self, step: int, timestep: float, action, x_in, x_out, flags: int = 0):
         xc_forward_chunk(self.h, step, timestep, action, x_in, x_out, flags)
+
+    def set_condition(self, cond):
+        xc_set_condition(self.h, cond)
 
     def kv_update(self, timestep: float, action, x_clean, x_out=None):
         xc_kv_update(self.h, timestep, action, x_clean, x_out)

@@ -45,12 +45,19 @@ class Lockstep:
         self.xc = XCache(self.m, w.gate, self.blob, self.stream)
         self.orc = xo.XCacheOracle(self.m, w.gate, self.blob, compute)
         self.seed = seed
+        if self.m.cond_len > 0:
+            self.set_condition(synth.condition_tokens(self.m, seed))
         self.band_hits = 0
         self.decisions_checked = 0
         self.worst = {}
 
     def close(self):
         self.xc.close()
+
+    def set_condition(self, cond):
+        """Same cross-attention condition tokens on both sides."""
+        self.xc.set_condition(cond)
+        self.orc.set_condition(cond)
 
     def _decide(self, gpu_dec, log):
         tau_dev = self.w.gate.tau_dev
@@ -82,10 +89,12 @@ class Lockstep:
             self.worst[tag] = max(self.worst.get(tag, 0.0), err)
             assert err <= tol_rel_l2, f"{tag}: rel-L2 {err:.3e} > {tol_rel_l2:.1e}"
 
-    def run(self, n_chunks, tol_abs=None, tol_rel_l2=None, flags=lambda n, t: 0, on_pass=None, kv_out=True):
+    def run(self, n_chunks, tol_abs=None, tol_rel_l2=None, flags=lambda n, t: 0, on_pass=None, kv_out=True,
+            cond_fn=None):
         """kv_out=False hands the KV-update pass no output buffer (the library then
         stops the last block after its key/value projection); the next chunks
-        still check that the committed keys/values are right."""
+        still check that the committed keys/values are right.  cond_fn(n), when
+        given, may return new condition tokens before chunk n (None: keep)."""
         torch = self.torch
         m, w = self.m, self.w
         L, C = m.tokens, m.hidden
@@ -97,6 +106,10 @@ class Lockstep:
         y_d = torch.empty_like(x_d)
         k_d = torch.empty_like(x_d)
         for n, eps, a in zip(range(n_chunks), eps_list, act_list):
+            if cond_fn is not None:
+                c = cond_fn(n)
+                if c is not None:
+                    self.set_condition(c)
             eps_d = torch.from_numpy(eps).to(dev)
             x_d.copy_(eps_d)
             x_o = eps.astype(np.float64)

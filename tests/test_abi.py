@@ -62,6 +62,13 @@ W0 = synth.workload(0)
     (dict(groups=(synth.ViewGroup(1, 0, 4, 4),)), xcp.XC_ERR_INVALID_ARG),
     (dict(dtype="bf16"), xcp.XC_ERR_UNSUPPORTED),         # head_dim 32 has no bf16 MFMA path
     (dict(n_heads=1, head_dim=256, hidden=256), xcp.XC_ERR_UNSUPPORTED),
+    (dict(rope=2), xcp.XC_ERR_INVALID_ARG),
+    (dict(rope=1, rope_theta=1.0), xcp.XC_ERR_INVALID_ARG),
+    (dict(rope=1, rope_theta=math.nan), xcp.XC_ERR_INVALID_ARG),
+    (dict(rope=1, groups=(synth.ViewGroup(1, 1, 1024, 1),)), xcp.XC_ERR_INVALID_ARG),
+    (dict(rope=1, n_heads=8, head_dim=15, hidden=120), xcp.XC_ERR_INVALID_ARG),   # odd head_dim
+    (dict(cond_len=-1), xcp.XC_ERR_INVALID_ARG),
+    (dict(cond_len=4097), xcp.XC_ERR_INVALID_ARG),
 ])
 def test_init_rejects_bad_model(change, want):
     m = synth.with_model(W0, **change).model
@@ -111,6 +118,13 @@ def test_calls_on_null_handle():
     assert lib.xc_destroy(None) == xcp.XC_OK
     assert lib.xc_axpby(None, 1.0, 1, 1.0, 1, 1, 4) == xcp.XC_ERR_INVALID_ARG
     assert lib.xc_profile(None, 1) == xcp.XC_ERR_INVALID_ARG
+    assert lib.xc_set_condition(None, a.ctypes.data, 1) == xcp.XC_ERR_INVALID_ARG
+
+
+def test_weight_blob_size_includes_cross_attention_tensors():
+    m = synth.with_model(W0, cond_len=16).model
+    short = np.zeros(synth.weights_numel(W0.model), np.float32)   # the blob without the cross tensors
+    assert _init_status(m, W0.gate, short) == xcp.XC_ERR_INVALID_ARG
 
 
 def _variants():

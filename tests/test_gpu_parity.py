@@ -265,3 +265,101 @@ def test_bf16_persistent_gemm_widths():
         ls.run(4, tol_rel_l2=TOLBF)
     finally:
         ls.close()
+
+
+# ---- WAN-style block extensions: 3-D rotary embedding and cross-attention ---------
+
+EXT_VARIANTS = {
+    "fp32-rope": synth.with_model(W0, rope=1),
+    "fp32-cross": synth.with_model(W0, cond_len=8),
+    "fp32-rope-cross-table1": synth.with_stream(synth.with_model(
+        synth.with_gate(W0, adaptive=1, tau_floor=0.97, tau_dev=2.0), rope=1, cond_len=8), rho=0.999),
+    "fp32-rope-cross-always-skip": synth.with_model(
+        synth.with_gate(W0, adaptive=0, tau_cos_fixed=-1.0, tau_dev=math.inf), rope=1, cond_len=8),
+    "fp32-rope-two-groups": synth.with_stream(synth.with_model(
+        synth.with_gate(W0, adaptive=1, tau_floor=0.97, tau_dev=2.0), rope=1, cond_len=5,
+        groups=(synth.ViewGroup(1, 2, 4, 4), synth.ViewGroup(2, 1, 3, 5))), rho=0.999),
+}
+
+
+@pytest.mark.parametrize("name", list(EXT_VARIANTS))
+def test_extension_fp32_variants(name):
+    """Rotary embedding and cross-attention on the tiny float32 model, pass by
+    pass, with the condition replaced (and its token count changed) mid-rollout."""
+    w = EXT_VARIANTS[name]
+    ls = _ls(w)
+    try:
+        m = w.model
+        cond_fn = None
+        if m.cond_len > 0:
+            cond_fn = lambda n: synth.condition_tokens(m, 10 + n, n_tokens=1 + (3 * n) % m.cond_len) \
+                if n in (2, 4) else None
+        st = ls.run(w.stream.n_chunks, tol_abs=TOL32, cond_fn=cond_fn)
+        print(f"[parity] {name} skips={st['skips']} band={ls.band_hits} worst={max(ls.worst.values()):.2e}",
+              flush=True)
+    finally:
+        ls.close()
+
+
+BF_EXT = synth.with_model(BF_RAGGED, rope=1, cond_len=77)
+
+
+def test_extension_bf16_ragged_parity():
+    """bf16, head_dim 128, L = 300 and 77 condition tokens (ragged against the
+    tiles), rotary embedding over a 3-chunk window, natural skips; the
+    condition is replaced by 64 tokens before chunk 2 and by 5 before chunk 3."""
+    ls = _ls(BF_EXT)
+    try:
+        m = BF_EXT.model
+        cond_fn = lambda n: {2: synth.condition_tokens(m, 21, n_tokens=64),
+                             3: synth.condition_tokens(m, 22, n_tokens=5)}.get(n)
+        st = ls.run(5, tol_rel_l2=TOLBF, cond_fn=cond_fn)
+        print(f"[parity] bf16-ext skips={st['skips']} band={ls.band_hits} worst={max(ls.worst.values()):.2e}",
+              flush=True)
+        assert st["skips"] > 0
+    finally:
+        ls.close()
+
+
+def test_extension_bf16_head64_kv_without_output():
+    w = synth.with_model(BF_RAGGED, n_heads=4, head_dim=64, groups=(synth.ViewGroup(1, 3, 7, 9),), rope=1,
+                         cond_len=33)
+    ls = _ls(w)
+    try:
+        ls.run(4, tol_rel_l2=TOLBF, kv_out=False)
+    finally:
+        ls.close()
+
+
+def test_condition_required_and_validated():
+    _need_gpu()
+    from paper_2604_20289_amd import xcache as xcp
+    w = synth.with_model(W0, cond_len=4)
+    dev = torch.device("cuda")
+    xc = xcp.XCache(w.model, w.gate, synth.make_weights(w.model), torch.cuda.current_stream().cuda_stream)
+    try:
+        x = torch.zeros((w.model.tokens, w.model.hidden), dtype=torch.float32, device=dev)
+        a = np.zeros(w.model.action_dim, np.float32)
+        with pytest.raises(xcp.XCacheError) as e:
+            xc.forward_chunk(0, 1000.0, a, x, x)
+        assert e.value.status == xcp.XC_ERR_STATE
+        with pytest.raises(xcp.XCacheError) as e:
+            xc.set_condition(np.zeros((5, w.model.hidden), np.float32))     # more than cond_len
+        assert e.value.status == xcp.XC_ERR_INVALID_ARG
+        bad = np.zeros((2, w.model.hidden), np.float32)
+        bad[1, 3] = np.nan
+        with pytest.raises(xcp.XCacheError) as e:
+            xc.set_condition(bad)
+        assert e.value.status == xcp.XC_ERR_INVALID_ARG
+        xc.set_condition(np.ones((4, w.model.hidden), np.float32))
+        xc.forward_chunk(0, 1000.0, a, x, x)
+        torch.cuda.synchronize()
+    finally:
+        xc.close()
+    plain = xcp.XCache(W0.model, W0.gate, synth.make_weights(W0.model), torch.cuda.current_stream().cuda_stream)
+    try:
+        with pytest.raises(xcp.XCacheError) as e:
+            plain.set_condition(np.ones((1, W0.model.hidden), np.float32))
+        assert e.value.status == xcp.XC_ERR_STATE
+    finally:
+        plain.close()
