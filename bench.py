@@ -70,7 +70,10 @@ def log(msg):
 
 def block_flops(m, n_keys):
     L, C, Dm = m.tokens, m.hidden, m.mlp_hidden
-    return 6.0 * L * C * C + 2.0 * L * C * C + 4.0 * L * C * Dm + 4.0 * L * n_keys * C
+    f = 6.0 * L * C * C + 2.0 * L * C * C + 4.0 * L * C * Dm + 4.0 * L * n_keys * C
+    if m.cond_len > 0:  # cross-attention: q and output projections, attention over the condition
+        f += 4.0 * L * C * C + 4.0 * L * m.cond_len * C
+    return f
 
 
 def attention_flops(m, n_keys):
@@ -138,6 +141,8 @@ def cpu_baseline(w, weights, seed):
     small = synth.with_model(w, n_blocks=1).model
     blob = weights[: synth.block_numel(m)]
     orc = xo.XCacheOracle(small, synth.GateParams(enabled=0), blob)
+    if m.cond_len > 0:
+        orc.set_condition(synth.condition_tokens(m, seed))
     rng = np.random.default_rng(seed + 7)
     L, H, d = m.tokens, m.n_heads, m.head_dim
     orc.ring[0] = [(xo.bf16_round(rng.standard_normal((H, L, d))), xo.bf16_round(rng.standard_normal((H, L, d))))
@@ -165,9 +170,10 @@ def cpu_baseline(w, weights, seed):
                        f"{m.n_blocks * (m.n_steps + 1)} block evaluations to a full-compute chunk")}
 
 
-def ablations(w, m, weights, eps_dev, actions, stream, args, xcp, torch):
+def ablations(w, m, weights, eps_dev, actions, make_xc, args, torch):
     """Synthetic analogues of the paper's gate ablations (Section 4.4): the same stream under
     step-0 handling, anchor, staleness, refresh and threshold variants; skip rate and latency only."""
+    from paper_2604_20289_amd import xcache as xcp
     variants = [
         ("table1", {}),
         ("step0_force", {"step0_mode": xcp.XC_STEP0_FORCE}),
@@ -183,7 +189,7 @@ def ablations(w, m, weights, eps_dev, actions, stream, args, xcp, torch):
     B, S = m.n_blocks, m.n_steps
     for name, kw in variants:
         wv = synth.with_gate(w, **kw)
-        xc = xcp.XCache(m, wv.gate, weights, stream)
+        xc = make_xc(wv.gate)
         ms = [v[0] for v in run_stream(xc, m, eps_dev, actions, args.warmup, args.steps, torch)]
         st = xc.stats()
         xc.close()
@@ -214,6 +220,10 @@ def main():
                     help="instead of the benchmark line, print one line of gate ablations on the same stream: "
                          "step-0 modes, anchors, staleness bound, refresh mode and a tau_floor sweep (skip rate "
                          "and mean chunk latency of each; --steps timed chunks after --warmup)")
+    ap.add_argument("--rope", action="store_true",
+                    help="model with the 3-D rotary embedding of the self-attention queries and keys")
+    ap.add_argument("--cond-len", type=int, default=0,
+                    help="model with a cross-attention layer over this many condition tokens")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="copy a buffer of this many MiB once (calibrates rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     args = ap.parse_args()
@@ -233,6 +243,10 @@ def main():
     w = synth.workload(args.workload)
     if args.tau_floor is not None:
         w = synth.with_gate(w, tau_floor=args.tau_floor)
+    if args.rope or args.cond_len:
+        w = synth.with_model(w, rope=int(args.rope), cond_len=args.cond_len)
+        w = synth.Workload(w.name + ("-rope" if args.rope else "") +
+                           (f"-cross{args.cond_len}" if args.cond_len else ""), w.model, w.gate, w.stream)
     m = w.model
     n_chunks = args.warmup + args.steps
     log(f"workload {w.name}: L={m.tokens} blocks={m.n_blocks} chunks={n_chunks}")
@@ -244,6 +258,14 @@ def main():
     del eps_host
     log(f"inputs ready in {time.time() - t0:.1f} s")
     stream = torch.cuda.current_stream().cuda_stream
+    cond = synth.condition_tokens(m, args.seed) if m.cond_len > 0 else None
+
+    def make_xc(gate):
+        xc = xcp.XCache(m, gate, weights, stream)
+        if cond is not None:
+            xc.set_condition(cond)
+        return xc
+
     if args.calib_copy_mib:
         n = args.calib_copy_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")
@@ -255,11 +277,11 @@ def main():
         del src, dst
 
     if args.ablations:
-        print(json.dumps(ablations(w, m, weights, eps_dev, actions, stream, args, xcp, torch)), flush=True)
+        print(json.dumps(ablations(w, m, weights, eps_dev, actions, make_xc, args, torch)), flush=True)
         return
 
     # 1. gate on
-    xc = xcp.XCache(m, w.gate, weights, stream)
+    xc = make_xc(w.gate)
     on_split = run_stream(xc, m, eps_dev, actions, args.warmup, args.steps, torch)
     on_ms = [v[0] for v in on_split]
     st = xc.stats()
@@ -276,7 +298,7 @@ def main():
     alt = None
     if args.tau_floor is None and not args.no_alt_tau:
         wa = synth.with_gate(w, tau_floor=0.95)
-        xc = xcp.XCache(m, wa.gate, weights, stream)
+        xc = make_xc(wa.gate)
         alt_ms = [v[0] for v in run_stream(xc, m, eps_dev, actions, args.warmup, args.steps, torch)]
         sa = xc.stats()
         xc.close()
@@ -288,7 +310,7 @@ def main():
     # 1c. periodic whole-generation refresh: skip fraction per chunk
     cadence = None
     if args.force_every > 0:
-        xc = xcp.XCache(m, w.gate, weights, stream)
+        xc = make_xc(w.gate)
         counts = []
         cad_ms = [v[0] for v in run_stream(xc, m, eps_dev, actions, 0, n_chunks, torch,
                                            force_every=args.force_every, per_chunk=counts)]
@@ -302,7 +324,7 @@ def main():
     # 2. gate off
     off_ms, kt = None, {}
     if not args.no_gate_off:
-        xc = xcp.XCache(m, synth.with_gate(w, enabled=0).gate, weights, stream)
+        xc = make_xc(synth.with_gate(w, enabled=0).gate)
         off_ms = [v[0] for v in run_stream(xc, m, eps_dev, actions, args.warmup, args.steps, torch, profile=True)]
         kt = kernel_table(xc, xcp)
         xc.close()
@@ -331,6 +353,7 @@ def main():
         "config": {"workload": w.name, "blocks": B, "hidden": m.hidden, "heads": m.n_heads,
                    "head_dim": m.head_dim, "mlp_hidden": m.mlp_hidden, "tokens_per_chunk": m.tokens,
                    "kv_window_chunks": m.kv_window, "keys": Lk, "denoising_steps": S,
+                   "rope": m.rope, "cross_attention_tokens": m.cond_len,
                    "stream_rho": w.stream.rho, "gate": "Table 1 defaults" if args.tau_floor is None
                    else f"Table 1 with tau_floor={args.tau_floor}", "steady_state_window": steady},
         "chunk_ms_median": round(statistics.median(on_ms), 3),
@@ -358,7 +381,8 @@ def main():
         res["block_tflops_effective"] = round(chunk_flops / (off_mean * 1e-3) / 1e12, 1)
         res["block_mfma_frac_effective"] = round(res["block_tflops_effective"] / PEAK_BF16_TFLOPS, 4)
         contraction_ms = sum(kt[k]["total_ms"] for k in ("attention", "gemm_qkv", "gemm_oproj", "gemm_up",
-                                                         "gemm_down") if k in kt)
+                                                         "gemm_down", "cross_q", "cross_attention", "cross_o")
+                             if k in kt)
         n_blocks_timed = args.steps * B * (S + 1)
         if contraction_ms > 0:
             res["block_tflops_kernels"] = round(fl_block * n_blocks_timed / (contraction_ms * 1e-3) / 1e12, 1)
@@ -379,6 +403,10 @@ def main():
                 e["tflops"] = round(f / (v["avg_us"] * 1e-6) / 1e12, 1)
             if k == "attention":
                 e["tflops"] = res["roofline"]["achieved"]
+            if k == "cross_attention":
+                e["tflops"] = round(attention_flops(m, m.cond_len) / (v["avg_us"] * 1e-6) / 1e12, 1)
+            if k == "cross_o":
+                e["tflops"] = round(2.0 * m.tokens * m.hidden * m.hidden / (v["avg_us"] * 1e-6) / 1e12, 1)
             if k == "ln_mod":
                 e["gbs"] = round(6.0 * m.tokens * m.hidden / (v["avg_us"] * 1e-6) / 1e9, 1)
             res["kernels_full_compute"][k] = e

@@ -95,7 +95,7 @@ typedef struct xc_view_group {
  *     by p * rope_theta^(-2i/d_a); the first d - 4 floor(d/6) dimensions follow
  *     the frame position n*F + f (absolute across chunks, n the generation),
  *     the next 2 floor(d/6) the row h, the last 2 floor(d/6) the column w of
- *     the token in its camera's grid.  Needs head_dim even and >= 6,
+ *     the token in its camera's grid.  Needs head_dim even,
  *     rope_theta > 1, and every grid dimension < 1024.
  *   cond_len > 0: a cross-attention layer between the self-attention and the
  *     MLP: x1 += Wo_c softmax(q_c k_c^T / sqrt(d)) v_c + bo_c with

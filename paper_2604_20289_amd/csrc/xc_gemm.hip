@@ -243,31 +243,80 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(const bf16* __restric
       __syncthreads();
       const float* gain = part == 0 ? e.gq : e.gk;
       const bool rope = e.rope.tab != nullptr;
+      // rotary embedding, per column of this lane: the table entry of its pair
+      // at axis position 0, the entry stride per position, the position's bit
+      // offset in the packed row coordinates
+      int rbase[NT], rstride[NT], rshift[NT];
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const int tcol = wn * NT * 32 + nt * 32 + lo;
+        int pair = (tcol - (tcol / e.D) * e.D) >> 1, a = 0;
+        if (pair >= e.rope.np[0]) {
+          pair -= e.rope.np[0];
+          a = 1;
+          if (pair >= e.rope.np[1]) {
+            pair -= e.rope.np[1];
+            a = 2;
+          }
+        }
+        rbase[nt] = e.rope.off[a] + pair;
+        rstride[nt] = e.rope.np[a];
+        rshift[nt] = 10 * a;
+      }
+      // normalise (and rotate) in place first, store afterwards: no store sits
+      // between the table loads, whose waits would otherwise also wait for it
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int g = 0; g < 4; ++g)
+        for (int g = 0; g < 4; ++g) {
+          // the table entries of this group of 4 rows are loaded together (one wait, not one per value)
+          float2 cs[4][NT];
+          if (rope) {
+            int packed[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r)  // rows past M: clamped, never stored
+              packed[r] = e.rope.pos[min(m0 + wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r, M - 1)];
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+#pragma unroll
+              for (int nt = 0; nt < NT; ++nt)
+                cs[r][nt] = e.rope.tab[rbase[nt] + ((packed[r] >> rshift[nt]) & 1023) * rstride[nt]];
+          }
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int trow = wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r;
-            const int row = m0 + trow;
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) {
               const int tcol = wn * NT * 32 + nt * 32 + lo;
               const int hd = tcol / e.D, dd = tcol - hd * e.D;
               float v = acc[mt][nt][g * 4 + r] * ss[trow * 65 + 64 - hd] * gain[dd];
               if (rope) {
-                // rotary pair (dd & ~1, dd | 1) = lanes (lo & ~1, lo | 1) of the same row:
-                // (a, b) -> (a c - b s, a s + b c); rows past M use a clamped table row
-                const float pv = __shfl_xor(v, 1, 64);
-                const float2 cs = rope_cs(e.rope, min(row, M - 1), dd >> 1);
-                v = v * cs.x + ((lo & 1) ? pv : -pv) * cs.y;
+                // rotary pair (dd & ~1, dd | 1) = lanes (lo & ~1, lo | 1) of the same row, swapped
+                // by a DPP quad permutation [1, 0, 3, 2]: (a, b) -> (a c - b s, a s + b c)
+                const float pv = __builtin_bit_cast(
+                    float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
+                v = v * cs[r][nt].x + ((lo & 1) ? pv : -pv) * cs[r][nt].y;
               }
-              if (row >= M) continue;
+              acc[mt][nt][g * 4 + r] = v;
+            }
+          }
+        }
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int row = m0 + wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r;
+            if (row >= M) continue;
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+              const int tcol = wn * NT * 32 + nt * 32 + lo;
+              const int hd = tcol / e.D, dd = tcol - hd * e.D;
               const long long hh = head0 + hd;
               bf16* dst = part == 0 ? reinterpret_cast<bf16*>(e.q_out) + (hh * e.Mpad + row) * e.D + dd
                                     : reinterpret_cast<bf16*>(e.k_cache) + (hh * e.Lcap + e.kv_off + row) * e.D + dd;
-              *dst = (bf16)v;
+              *dst = (bf16)acc[mt][nt][g * 4 + r];
             }
           }
     } else {

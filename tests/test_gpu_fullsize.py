@@ -135,3 +135,55 @@ def test_large_multicamera_fullsize_one_block():
         assert err <= 2e-2
     finally:
         xc.close()
+
+
+def test_multicamera_extended_block_fullsize():
+    """The multi-camera shapes with both block extensions (3-D rotary embedding,
+    cross-attention to 512 condition tokens), one gated block: chunk 0 in full,
+    then the KV-update pass and chunk 1 step 0 (14040 keys, frame positions 3-5
+    against the cached 0-2) on sampled token rows.  Relative L2 2e-2."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from lockstep import in_band, rel_l2
+    from paper_2604_20289_amd.xcache import XCache
+
+    w = synth.with_model(synth.with_gate(synth.workload(2), front_anchors=0), n_blocks=1, rope=1, cond_len=512)
+    m = w.model
+    L = m.tokens
+    rows = np.unique(np.concatenate([np.linspace(0, L - 1, 89).astype(int), np.arange(0, L, 1170)]))
+    blob = synth.make_weights(m)
+    cond = synth.condition_tokens(m, 0)
+    print(f"[fullsize-ext] L={L} C={m.hidden} cond={cond.shape[0]} rows checked={len(rows)}", flush=True)
+    xc = XCache(m, w.gate, blob, torch.cuda.current_stream().cuda_stream)
+    orc = xo.XCacheOracle(m, w.gate, blob, compute=np.float32)
+    xc.set_condition(cond)
+    orc.set_condition(cond)
+    eps = list(synth.latent_stream(m, w.stream, 0, 2))
+    acts = list(synth.action_stream(m, w.stream, 0, 2))
+    taus = synth.timesteps(m)
+    try:
+        dev = torch.device("cuda")
+        y = torch.empty((L, m.hidden), dtype=torch.float32, device=dev)
+        xc.forward_chunk(0, taus[0], acts[0], torch.from_numpy(eps[0]).to(dev), y)
+        yo = orc.forward_chunk(0, taus[0], acts[0], eps[0])
+        err = rel_l2(y.cpu().numpy()[rows], yo[rows])
+        print(f"[fullsize-ext] chunk 0 step 0 rel-L2 on sampled rows {err:.2e}", flush=True)
+        assert err <= 2e-2
+        xc.kv_update(0.0, acts[0], y)
+        orc.kv_update(0.0, acts[0], yo, rows=rows)
+        xc.forward_chunk(0, taus[0], acts[1], torch.from_numpy(eps[1]).to(dev), y)
+        st = xc.stats()
+
+        def decide(b, info):
+            dev_skip = int(st["last_decision"][b]) == xo.DEC_SKIP
+            if dev_skip != bool(info["skip"]):
+                assert in_band(info, w.gate.tau_dev), (b, info, st["last_cos"][b], st["last_dev"][b])
+            return dev_skip
+
+        yo1 = orc.forward_chunk(0, taus[0], acts[1], eps[1], decide=decide, rows=rows)
+        err = rel_l2(y.cpu().numpy()[rows], yo1)
+        print(f"[fullsize-ext] chunk 1 step 0 decision={st['last_decision'][0]} rel-L2 on sampled rows {err:.2e}",
+              flush=True)
+        assert err <= 2e-2
+    finally:
+        xc.close()
