@@ -407,66 +407,75 @@ __device__ __forceinline__ void grouped_tile(int j, int n_tm, int n_tn, int& tm,
 
 // Epilogue of the persistent kernel for the element-wise modes.  The lane's
 // rows are r0 + mt*32 + g*8 + r, its columns cb + nt*32.  Column constants
-// (bias, gate) are read once; each row's operand loads are issued together
-// before its stores; rows past M are never stored (their loads use a clamped
-// row).  Blocks of 4 rows are processed one at a time, which bounds the live
-// registers.
+// (bias, gate) are read once.  The 16 blocks of 4 rows are processed one at
+// a time (which bounds the live registers) and software-pipelined: the
+// operand loads of block k+1 (residual, block input) are issued before block
+// k is computed and stored, so the HBM latency of one block overlaps the
+// work of the previous one instead of being paid 16 times in a row.  Rows
+// past M are never stored (their loads use a clamped row).
 template <int MODE, int NT>
 __device__ __forceinline__ void persistent_epilogue(const EpiArgs& e, const f32x16 (&acc)[4][NT], int r0, int cb,
                                                     int M) {
+  constexpr bool kRes = MODE == EPI_OPROJ || MODE == EPI_DOWN;
+  constexpr bool kXin = MODE == EPI_DOWN;
   float bias[NT], gate[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     bias[nt] = e.bias[cb + nt * 32];
-    gate[nt] = (MODE == EPI_OPROJ || MODE == EPI_DOWN) ? e.gate[cb + nt * 32] : 0.f;
+    gate[nt] = kRes ? e.gate[cb + nt * 32] : 0.f;
   }
   const long long N = e.N;
+  float res[2][4][NT], xin[2][4][NT];
+  auto load = [&](int blk, int slot) __attribute__((always_inline)) {
+    const int mt = blk >> 2, g = blk & 3;
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt)
+    for (int r = 0; r < 4; ++r) {
+      const long long il = (long long)min(r0 + mt * 32 + g * 8 + r, M - 1) * N + cb;
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      // this block's 4 x NT accumulators move to VGPRs here, not all at once
-      float v[4][NT];
+      for (int nt = 0; nt < NT; ++nt) {
+        if constexpr (kRes) res[slot][r][nt] = e.resid[il + nt * 32];
+        if constexpr (kXin) xin[slot][r][nt] = e.xin[il + nt * 32];
+      }
+    }
+  };
+  load(0, 0);
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
+  for (int blk = 0; blk < 16; ++blk) {
+    const int mt = blk >> 2, g = blk & 3, slot = blk & 1;
+    if (blk + 1 < 16) load(blk + 1, slot ^ 1);
+    __builtin_amdgcn_sched_barrier(0);
+    // this block's 4 x NT accumulators move to VGPRs here, not all at once
+    float v[4][NT];
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          v[r][nt] = acc[mt][nt][g * 4 + r];
-          asm volatile("" : "+v"(v[r][nt]));
-        }
+    for (int r = 0; r < 4; ++r)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = r0 + mt * 32 + g * 8 + r;
-        const long long il = (long long)min(row, M - 1) * N + cb;
-        const long long is = (long long)row * N + cb;
-        float res[NT], xin[NT];
-        if constexpr (MODE == EPI_OPROJ || MODE == EPI_DOWN) {
+      for (int nt = 0; nt < NT; ++nt) {
+        v[r][nt] = acc[mt][nt][g * 4 + r];
+        asm volatile("" : "+v"(v[r][nt]));
+      }
 #pragma unroll
-          for (int nt = 0; nt < NT; ++nt) res[nt] = e.resid[il + nt * 32];
-        }
-        if constexpr (MODE == EPI_DOWN) {
+    for (int r = 0; r < 4; ++r) {
+      const int row = r0 + mt * 32 + g * 8 + r;
+      const long long is = (long long)row * N + cb;
+      if (row >= M) continue;
 #pragma unroll
-          for (int nt = 0; nt < NT; ++nt) xin[nt] = e.xin[il + nt * 32];
-        }
-        if (row >= M) continue;
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          const float x = v[r][nt] + bias[nt];
-          if constexpr (MODE == EPI_BIAS_F32) {
-            e.out_f32[is + nt * 32] = x;
-          } else if constexpr (MODE == EPI_OPROJ) {
-            e.out_f32[is + nt * 32] = res[nt] + gate[nt] * x;
-          } else if constexpr (MODE == EPI_UP) {
-            reinterpret_cast<bf16*>(e.out_t)[is + nt * 32] = (bf16)gelu_tanh(x);
-          } else if constexpr (MODE == EPI_DOWN) {
-            const float y = res[nt] + gate[nt] * x;
-            e.out_f32[is + nt * 32] = y;
-            if (e.out_t != nullptr) reinterpret_cast<bf16*>(e.out_t)[is + nt * 32] = (bf16)(y - xin[nt]);
-          }
+      for (int nt = 0; nt < NT; ++nt) {
+        const float x = v[r][nt] + bias[nt];
+        if constexpr (MODE == EPI_BIAS_F32) {
+          e.out_f32[is + nt * 32] = x;
+        } else if constexpr (MODE == EPI_OPROJ) {
+          e.out_f32[is + nt * 32] = res[slot][r][nt] + gate[nt] * x;
+        } else if constexpr (MODE == EPI_UP) {
+          reinterpret_cast<bf16*>(e.out_t)[is + nt * 32] = (bf16)gelu_tanh(x);
+        } else if constexpr (MODE == EPI_DOWN) {
+          const float y = res[slot][r][nt] + gate[nt] * x;
+          e.out_f32[is + nt * 32] = y;
+          if (e.out_t != nullptr) reinterpret_cast<bf16*>(e.out_t)[is + nt * 32] = (bf16)(y - xin[slot][r][nt]);
         }
       }
-      __builtin_amdgcn_sched_barrier(0);
     }
+    __builtin_amdgcn_sched_barrier(0);
+  }
 }
 
 // vmcnt(n) lgkmcnt(0) (gfx9 encoding, expcnt left at its maximum)
