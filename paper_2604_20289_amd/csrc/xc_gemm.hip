@@ -411,13 +411,26 @@ __device__ __forceinline__ void grouped_tile(int j, int n_tm, int n_tn, int& tm,
 // a time (which bounds the live registers) and software-pipelined: the
 // operand loads of block k+1 (residual, block input) are issued before block
 // k is computed and stored, so the HBM latency of one block overlaps the
-// work of the previous one instead of being paid 16 times in a row.  Rows
-// past M are never stored (their loads use a clamped row).
+// work of the previous one instead of being paid 16 times in a row.  Stores
+// go through buffer descriptors whose range ends at row M (a store past it is
+// dropped by the hardware), so no branch separates them: the compiler then
+// knows how many stores follow each load batch and waits only for the loads
+// it needs, not for every earlier store.  Loads of rows past M use a clamped
+// row.  tile_rows: rows of this tile, r0 the lane's first row relative to it.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(void* base, long long bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(base, (short)0, (int)bytes, 0x00020000);
+}
+
 template <int MODE, int NT>
-__device__ __forceinline__ void persistent_epilogue(const EpiArgs& e, const f32x16 (&acc)[4][NT], int r0, int cb,
-                                                    int M) {
+__device__ __forceinline__ void persistent_epilogue(const EpiArgs& e, const f32x16 (&acc)[4][NT], int m0, int r0,
+                                                    int cb, int M) {
   constexpr bool kRes = MODE == EPI_OPROJ || MODE == EPI_DOWN;
   constexpr bool kXin = MODE == EPI_DOWN;
+  // the tile's rows [m0, min(m0 + PBM, M)) of every output, as buffer ranges
+  const long long rows = min(PBM, M - m0);
+  const __amdgpu_buffer_rsrc_t out_f = tile_rsrc(e.out_f32 + (long long)m0 * e.N, rows * e.N * 4);
+  const __amdgpu_buffer_rsrc_t out_b =
+      tile_rsrc(reinterpret_cast<bf16*>(e.out_t) + (long long)m0 * e.N, e.out_t != nullptr ? rows * e.N * 2 : 0);
   float bias[NT], gate[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
@@ -430,7 +443,7 @@ __device__ __forceinline__ void persistent_epilogue(const EpiArgs& e, const f32x
     const int mt = blk >> 2, g = blk & 3;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const long long il = (long long)min(r0 + mt * 32 + g * 8 + r, M - 1) * N + cb;
+      const long long il = (long long)min(m0 + r0 + mt * 32 + g * 8 + r, M - 1) * N + cb;
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         if constexpr (kRes) res[slot][r][nt] = e.resid[il + nt * 32];
@@ -455,22 +468,26 @@ __device__ __forceinline__ void persistent_epilogue(const EpiArgs& e, const f32x
       }
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int row = r0 + mt * 32 + g * 8 + r;
-      const long long is = (long long)row * N + cb;
-      if (row >= M) continue;
+      // element offset within the tile's rows (past the range: dropped)
+      const int is = (r0 + mt * 32 + g * 8 + r) * (int)N + cb;
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         const float x = v[r][nt] + bias[nt];
+        const int o = is + nt * 32;
         if constexpr (MODE == EPI_BIAS_F32) {
-          e.out_f32[is + nt * 32] = x;
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, x), out_f, o * 4, 0, 0);
         } else if constexpr (MODE == EPI_OPROJ) {
-          e.out_f32[is + nt * 32] = res[slot][r][nt] + gate[nt] * x;
+          const float y = res[slot][r][nt] + gate[nt] * x;
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, y), out_f, o * 4, 0, 0);
         } else if constexpr (MODE == EPI_UP) {
-          reinterpret_cast<bf16*>(e.out_t)[is + nt * 32] = (bf16)gelu_tanh(x);
+          const bf16 u = (bf16)gelu_tanh(x);
+          __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, u), out_b, o * 2, 0, 0);
         } else if constexpr (MODE == EPI_DOWN) {
           const float y = res[slot][r][nt] + gate[nt] * x;
-          e.out_f32[is + nt * 32] = y;
-          if (e.out_t != nullptr) reinterpret_cast<bf16*>(e.out_t)[is + nt * 32] = (bf16)(y - xin[slot][r][nt]);
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, y), out_f, o * 4, 0, 0);
+          const bf16 d = (bf16)(y - xin[slot][r][nt]);
+          // out_t == null: a zero-length range drops the cached-residual store
+          __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, d), out_b, o * 2, 0, 0);
         }
       }
     }
@@ -677,7 +694,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_persistent(const bf16* __res
     // accumulator element (mt, nt, g*4 + r): tile row wm*128 + mt*32 + g*8 + hi*4 + r,
     // tile column wn*32*NT + nt*32 + lo
     static_assert(MODE != EPI_QKV, "the fused QKV projection runs on the two-workgroup kernel");
-    persistent_epilogue<MODE, NT>(e, acc, m0 + rb, n0 + wn * NT * 32 + lo, M);
+    persistent_epilogue<MODE, NT>(e, acc, m0, rb, n0 + wn * NT * 32 + lo, M);
   }
   // no LDS request may still be landing when the workgroup retires
   XC_WAIT_VM_LGKM0(0);
