@@ -301,22 +301,35 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(const bf16* __restric
             }
           }
         }
+      // Stores: a wave's 32*NT columns lie in one head (NT*32 <= D), whose rows
+      // [m0, min(m0 + BM, M)) form one buffer range; the even lane of each
+      // column pair stores both values as one dword (the odd lane's offset is
+      // the range's end, so its store is dropped), and rows past M are dropped
+      // by the range check, so no branch separates the stores.
+      static_assert(NT * 32 <= 64, "one head per wave");
+      const int hd = (wn * NT * 32) / e.D;
+      const long long hh = head0 + hd;
+      const int rows = min(T::BM, M - m0);
+      bf16* hbase = part == 0 ? reinterpret_cast<bf16*>(e.q_out) + (hh * e.Mpad + m0) * e.D
+                              : reinterpret_cast<bf16*>(e.k_cache) + (hh * e.Lcap + e.kv_off + m0) * e.D;
+      const __amdgpu_buffer_rsrc_t dst = __builtin_amdgcn_make_buffer_rsrc(hbase, (short)0, rows * e.D * 2, 0x00020000);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int g = 0; g < 4; ++g)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const int row = m0 + wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r;
-            if (row >= M) continue;
+            const int trow = wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r;
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) {
-              const int tcol = wn * NT * 32 + nt * 32 + lo;
-              const int hd = tcol / e.D, dd = tcol - hd * e.D;
-              const long long hh = head0 + hd;
-              bf16* dst = part == 0 ? reinterpret_cast<bf16*>(e.q_out) + (hh * e.Mpad + row) * e.D + dd
-                                    : reinterpret_cast<bf16*>(e.k_cache) + (hh * e.Lcap + e.kv_off + row) * e.D + dd;
-              *dst = (bf16)acc[mt][nt][g * 4 + r];
+              const int dd = (wn * NT * 32 + nt * 32 + lo) - hd * e.D;
+              const float v = acc[mt][nt][g * 4 + r];
+              const float pv = __builtin_bit_cast(
+                  float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
+              const unsigned two = (unsigned)__builtin_bit_cast(unsigned short, (bf16)v) |
+                                   ((unsigned)__builtin_bit_cast(unsigned short, (bf16)pv) << 16);
+              const int off = (lo & 1) ? rows * e.D * 2 : (trow * e.D + dd) * 2;
+              __builtin_amdgcn_raw_buffer_store_b32(two, dst, off, 0, 0);
             }
           }
     } else {
