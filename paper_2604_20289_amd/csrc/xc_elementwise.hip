@@ -153,18 +153,21 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const float* __restrict__ x
   }
   const float var = wave_sum(q) / (float)C;
   const float rstd = 1.0f / sqrtf(var + 1e-6f);
-  T* orow = out + (long long)row * C;
+  // four consecutive outputs per lane leave as one 8-byte (bf16) or 16-byte store
+  typedef T T4 __attribute__((ext_vector_type(4)));
+  T4* orow = reinterpret_cast<T4*>(out + (long long)row * C);
 #pragma unroll
   for (int i = 0; i < MAXV; ++i) {
     int c4 = lane + i * 64;
     if (c4 < C4) {
       float4 sc = reinterpret_cast<const float4*>(scale)[c4];
       float4 sh = reinterpret_cast<const float4*>(shift)[c4];
-      int c = c4 * 4;
-      orow[c + 0] = to_t<T>((v[i].x - mu) * rstd * (1.f + sc.x) + sh.x);
-      orow[c + 1] = to_t<T>((v[i].y - mu) * rstd * (1.f + sc.y) + sh.y);
-      orow[c + 2] = to_t<T>((v[i].z - mu) * rstd * (1.f + sc.z) + sh.z);
-      orow[c + 3] = to_t<T>((v[i].w - mu) * rstd * (1.f + sc.w) + sh.w);
+      T4 o;
+      o[0] = to_t<T>((v[i].x - mu) * rstd * (1.f + sc.x) + sh.x);
+      o[1] = to_t<T>((v[i].y - mu) * rstd * (1.f + sc.y) + sh.y);
+      o[2] = to_t<T>((v[i].z - mu) * rstd * (1.f + sc.z) + sh.z);
+      o[3] = to_t<T>((v[i].w - mu) * rstd * (1.f + sc.w) + sh.w);
+      orow[c4] = o;
     }
   }
 }
