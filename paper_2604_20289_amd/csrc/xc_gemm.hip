@@ -62,6 +62,97 @@ __device__ __forceinline__ void epilogue(const EpiArgs& e, int m, int n, float a
   }
 }
 
+// Element-wise epilogue of an MT x NT block of 32x32 accumulators (both bf16
+// GEMM kernels).  The lane's rows are m0 + r0 + mt*32 + g*8 + r (m0 the tile's
+// first row, BM its height), its columns cb + nt*32.  Column constants
+// (bias, gate) are read once.  The 16 blocks of 4 rows are processed one at
+// a time (which bounds the live registers) and software-pipelined: the
+// operand loads of block k+1 (residual, block input) are issued before block
+// k is computed and stored, so the HBM latency of one block overlaps the
+// work of the previous one instead of being paid 16 times in a row.  Stores
+// go through buffer descriptors whose range ends at row M (a store past it is
+// dropped by the hardware), so no branch separates them: the compiler then
+// knows how many stores follow each load batch and waits only for the loads
+// it needs, not for every earlier store.  Loads of rows past M use a clamped
+// row.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(void* base, long long bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(base, (short)0, (int)bytes, 0x00020000);
+}
+
+template <int MODE, int MT, int NT>
+__device__ __forceinline__ void tile_epilogue(const EpiArgs& e, const f32x16 (&acc)[MT][NT], int m0, int r0, int cb,
+                                              int M, int BM) {
+  constexpr bool kRes = MODE == EPI_OPROJ || MODE == EPI_DOWN;
+  constexpr bool kXin = MODE == EPI_DOWN;
+  // the tile's rows [m0, min(m0 + PBM, M)) of every output, as buffer ranges
+  const long long rows = min(BM, M - m0);
+  const __amdgpu_buffer_rsrc_t out_f = tile_rsrc(e.out_f32 + (long long)m0 * e.N, rows * e.N * 4);
+  const __amdgpu_buffer_rsrc_t out_b =
+      tile_rsrc(reinterpret_cast<bf16*>(e.out_t) + (long long)m0 * e.N, e.out_t != nullptr ? rows * e.N * 2 : 0);
+  float bias[NT], gate[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    bias[nt] = e.bias[cb + nt * 32];
+    gate[nt] = kRes ? e.gate[cb + nt * 32] : 0.f;
+  }
+  const long long N = e.N;
+  float res[2][4][NT], xin[2][4][NT];
+  auto load = [&](int blk, int slot) __attribute__((always_inline)) {
+    const int mt = blk >> 2, g = blk & 3;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const long long il = (long long)min(m0 + r0 + mt * 32 + g * 8 + r, M - 1) * N + cb;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        if constexpr (kRes) res[slot][r][nt] = e.resid[il + nt * 32];
+        if constexpr (kXin) xin[slot][r][nt] = e.xin[il + nt * 32];
+      }
+    }
+  };
+  load(0, 0);
+#pragma unroll
+  for (int blk = 0; blk < 4 * MT; ++blk) {
+    const int mt = blk >> 2, g = blk & 3, slot = blk & 1;
+    if (blk + 1 < 4 * MT) load(blk + 1, slot ^ 1);
+    __builtin_amdgcn_sched_barrier(0);
+    // this block's 4 x NT accumulators move to VGPRs here, not all at once
+    float v[4][NT];
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        v[r][nt] = acc[mt][nt][g * 4 + r];
+        asm volatile("" : "+v"(v[r][nt]));
+      }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      // element offset within the tile's rows (past the range: dropped)
+      const int is = (r0 + mt * 32 + g * 8 + r) * (int)N + cb;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const float x = v[r][nt] + bias[nt];
+        const int o = is + nt * 32;
+        if constexpr (MODE == EPI_BIAS_F32) {
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, x), out_f, o * 4, 0, 0);
+        } else if constexpr (MODE == EPI_OPROJ) {
+          const float y = res[slot][r][nt] + gate[nt] * x;
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, y), out_f, o * 4, 0, 0);
+        } else if constexpr (MODE == EPI_UP) {
+          const bf16 u = (bf16)gelu_tanh(x);
+          __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, u), out_b, o * 2, 0, 0);
+        } else if constexpr (MODE == EPI_DOWN) {
+          const float y = res[slot][r][nt] + gate[nt] * x;
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, y), out_f, o * 4, 0, 0);
+          const bf16 d = (bf16)(y - xin[slot][r][nt]);
+          // out_t == null: a zero-length range drops the cached-residual store
+          __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, d), out_b, o * 2, 0, 0);
+        }
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // bf16 MFMA GEMM.  Workgroup = 4 waves in a 2x2 arrangement; a wave owns an
 // (MT*32) x (NT*32) sub-tile, i.e. MT x NT independent 32x32 accumulators of
@@ -368,18 +459,7 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(const bf16* __restric
       }
     }
   } else {
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-        for (int g = 0; g < 4; ++g)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int row = m0 + wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r;
-            const int col = n0 + wn * NT * 32 + nt * 32 + lo;
-            if (row < M) epilogue<MODE, bf16>(e, row, col, acc[mt][nt][g * 4 + r]);
-          }
+    tile_epilogue<MODE, MT, NT>(e, acc, m0, wm * MT * 32 + hi * 4, n0 + wn * NT * 32 + lo, M, T::BM);
   }
 }
 
@@ -416,96 +496,6 @@ __device__ __forceinline__ void grouped_tile(int j, int n_tm, int n_tn, int& tm,
   const int gm = min(GM, n_tm - first_m);
   tm = first_m + (j % in_group) % gm;
   tn = (j % in_group) / gm;
-}
-
-// Epilogue of the persistent kernel for the element-wise modes.  The lane's
-// rows are r0 + mt*32 + g*8 + r, its columns cb + nt*32.  Column constants
-// (bias, gate) are read once.  The 16 blocks of 4 rows are processed one at
-// a time (which bounds the live registers) and software-pipelined: the
-// operand loads of block k+1 (residual, block input) are issued before block
-// k is computed and stored, so the HBM latency of one block overlaps the
-// work of the previous one instead of being paid 16 times in a row.  Stores
-// go through buffer descriptors whose range ends at row M (a store past it is
-// dropped by the hardware), so no branch separates them: the compiler then
-// knows how many stores follow each load batch and waits only for the loads
-// it needs, not for every earlier store.  Loads of rows past M use a clamped
-// row.  tile_rows: rows of this tile, r0 the lane's first row relative to it.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(void* base, long long bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(base, (short)0, (int)bytes, 0x00020000);
-}
-
-template <int MODE, int NT>
-__device__ __forceinline__ void persistent_epilogue(const EpiArgs& e, const f32x16 (&acc)[4][NT], int m0, int r0,
-                                                    int cb, int M) {
-  constexpr bool kRes = MODE == EPI_OPROJ || MODE == EPI_DOWN;
-  constexpr bool kXin = MODE == EPI_DOWN;
-  // the tile's rows [m0, min(m0 + PBM, M)) of every output, as buffer ranges
-  const long long rows = min(PBM, M - m0);
-  const __amdgpu_buffer_rsrc_t out_f = tile_rsrc(e.out_f32 + (long long)m0 * e.N, rows * e.N * 4);
-  const __amdgpu_buffer_rsrc_t out_b =
-      tile_rsrc(reinterpret_cast<bf16*>(e.out_t) + (long long)m0 * e.N, e.out_t != nullptr ? rows * e.N * 2 : 0);
-  float bias[NT], gate[NT];
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    bias[nt] = e.bias[cb + nt * 32];
-    gate[nt] = kRes ? e.gate[cb + nt * 32] : 0.f;
-  }
-  const long long N = e.N;
-  float res[2][4][NT], xin[2][4][NT];
-  auto load = [&](int blk, int slot) __attribute__((always_inline)) {
-    const int mt = blk >> 2, g = blk & 3;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const long long il = (long long)min(m0 + r0 + mt * 32 + g * 8 + r, M - 1) * N + cb;
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        if constexpr (kRes) res[slot][r][nt] = e.resid[il + nt * 32];
-        if constexpr (kXin) xin[slot][r][nt] = e.xin[il + nt * 32];
-      }
-    }
-  };
-  load(0, 0);
-#pragma unroll
-  for (int blk = 0; blk < 16; ++blk) {
-    const int mt = blk >> 2, g = blk & 3, slot = blk & 1;
-    if (blk + 1 < 16) load(blk + 1, slot ^ 1);
-    __builtin_amdgcn_sched_barrier(0);
-    // this block's 4 x NT accumulators move to VGPRs here, not all at once
-    float v[4][NT];
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        v[r][nt] = acc[mt][nt][g * 4 + r];
-        asm volatile("" : "+v"(v[r][nt]));
-      }
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      // element offset within the tile's rows (past the range: dropped)
-      const int is = (r0 + mt * 32 + g * 8 + r) * (int)N + cb;
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const float x = v[r][nt] + bias[nt];
-        const int o = is + nt * 32;
-        if constexpr (MODE == EPI_BIAS_F32) {
-          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, x), out_f, o * 4, 0, 0);
-        } else if constexpr (MODE == EPI_OPROJ) {
-          const float y = res[slot][r][nt] + gate[nt] * x;
-          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, y), out_f, o * 4, 0, 0);
-        } else if constexpr (MODE == EPI_UP) {
-          const bf16 u = (bf16)gelu_tanh(x);
-          __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, u), out_b, o * 2, 0, 0);
-        } else if constexpr (MODE == EPI_DOWN) {
-          const float y = res[slot][r][nt] + gate[nt] * x;
-          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, y), out_f, o * 4, 0, 0);
-          const bf16 d = (bf16)(y - xin[slot][r][nt]);
-          // out_t == null: a zero-length range drops the cached-residual store
-          __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, d), out_b, o * 2, 0, 0);
-        }
-      }
-    }
-    __builtin_amdgcn_sched_barrier(0);
-  }
 }
 
 // vmcnt(n) lgkmcnt(0) (gfx9 encoding, expcnt left at its maximum)
@@ -707,7 +697,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_persistent(const bf16* __res
     // accumulator element (mt, nt, g*4 + r): tile row wm*128 + mt*32 + g*8 + hi*4 + r,
     // tile column wn*32*NT + nt*32 + lo
     static_assert(MODE != EPI_QKV, "the fused QKV projection runs on the two-workgroup kernel");
-    persistent_epilogue<MODE, NT>(e, acc, m0, rb, n0 + wn * NT * 32 + lo, M);
+    tile_epilogue<MODE, 4, NT>(e, acc, m0, rb, n0 + wn * NT * 32 + lo, M, PBM);
   }
   // no LDS request may still be landing when the workgroup retires
   XC_WAIT_VM_LGKM0(0);
