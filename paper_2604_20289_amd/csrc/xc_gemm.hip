@@ -11,6 +11,8 @@
 //  * gemm_bf16_persistent: 256 x 192 tiles, one persistent workgroup per CU
 //    streaming its tiles through a 4-deep LDS ring; used for the other
 //    projections.
+// Both run the element-wise epilogues through tile_epilogue (software-
+// pipelined operand loads, range-checked buffer stores).
 //
 // fp32 path: a plain LDS-tiled FMA GEMM (64x64 tiles, 4x4 per thread) used
 // for float32 models.
