@@ -415,9 +415,17 @@ def main():
     for k, v in gate_k.items():
         e = {"launches": v["launches"], "avg_us": round(v["avg_us"], 2)}
         if k == "gate":
-            # one read of x, the cached fingerprint read and the current one written
-            fp_rows = len(xcp.xc_fingerprint_rows(m, w.gate)) + sum(g.views for g in m.groups)
-            e["bytes"] = 4.0 * L * C + 8.0 * fp_rows * C
+            # the cached fingerprint read and the current one written, plus the
+            # global channel's source: one read of x, or (bf16 models whose
+            # cameras all have >= 32 tokens, every gated block but block 0)
+            # the MLP-down column-sum partials of the previous block
+            n_srows = len(xcp.xc_fingerprint_rows(m, w.gate))
+            fp_rows = n_srows + sum(g.views for g in m.groups)
+            folded = m.dtype == synth.BF16 and min(g.frames * g.height * g.width for g in m.groups) >= 32
+            n_rb = (L + 31) // 32
+            e["global_channel"] = "MLP-down column-sum partials" if folded else "one read of the block input"
+            e["bytes"] = (4.0 * n_srows * C + 8.0 * fp_rows * C + 16.0 * n_rb * C) if folded else \
+                (4.0 * L * C + 8.0 * fp_rows * C)
             e["gbs"] = round(e["bytes"] / (v["avg_us"] * 1e-6) / 1e9, 1)
             e["hbm_frac"] = round(e["gbs"] / PEAK_HBM_GBS, 4)
         if k == "skip_add":

@@ -72,6 +72,14 @@ struct xc_handle {
   void* wo_c = nullptr; float* bo_c = nullptr; float* ln3_shift = nullptr; float* ln3_scale = nullptr;
   void* kc_c = nullptr; void* vt_c = nullptr; void* cond_act = nullptr; float* cond_kv = nullptr;
   float* ones = nullptr;
+  // gate global channel from the MLP-down epilogue (bf16 models whose cameras
+  // all have >= 32 tokens): partials, 32-row-block tables, per-pass input sums
+  // and per-(t, b) residual sums
+  bool fold = false;
+  int n_rb = 0;
+  float* csum_part = nullptr;
+  int* rb_split = nullptr; int* rb_cam = nullptr; int* cam_rb_lo = nullptr; int* cam_rb_hi = nullptr;
+  double* csum_in = nullptr; double* csum_rhat = nullptr;
   // caches
   void* kc = nullptr; void* vt = nullptr; void* rhat = nullptr; float* fp = nullptr;
   float* fp_alt = nullptr;  // second fingerprint set of the refresh-on-compute mode
@@ -417,7 +425,7 @@ void cross_attention(xc_handle* h, int b, const int* flag) {
 // kv_only: stop after the key/value cache write (the block's output is not
 // needed: the last block of a KV-update pass whose caller takes no output).
 void compute_block(xc_handle* h, int b, const float* x, float* out, const int* flag, void* rhat_tb,
-                   long long kv_off, long long Lk, bool kv_only = false) {
+                   long long kv_off, long long Lk, bool kv_only = false, bool col_sums = false) {
   const int C = h->C, H = h->H, D = h->D, Dm = h->Dm;
   const int L = (int)h->L;
   const size_t esz = h->esz;
@@ -508,6 +516,11 @@ void compute_block(xc_handle* h, int b, const float* x, float* out, const int* f
     e.resid = h->x1;
     e.gate = gate2;
     e.xin = x;
+    if (col_sums && h->fold) {  // the next block's gate takes its global channel from these
+      e.csum_part = h->csum_part;
+      e.rb_split = h->rb_split;
+      e.n_rb = h->n_rb;
+    }
     launch_gemm(h->dtype, EPI_DOWN, h->u, wptr<void>(h->w2, (size_t)b * C * Dm, esz), L, C, Dm, e, flag, h->st);
   }
 }
@@ -565,6 +578,38 @@ void build_tables(xc_handle* h) {
   t.srows = d_rows;
   h->n_wg = gate_workgroups(h->C, h->n_srows, h->n_cams);
   h->fp_records = dalloc_t<double>(h, (size_t)h->n_wg * kMaxGroups * kFpRecord);
+
+  // 32-row-block tables of the folded global channel: each block spans at
+  // most two cameras when every camera has >= 32 tokens
+  bool ok = h->g.enabled && h->dtype == XC_BF16;
+  for (int v = 0; v < cam && ok; ++v) ok = cam_row_begin[v + 1] - cam_row_begin[v] >= 32;
+  h->fold = ok;
+  if (ok) {
+    const int L = (int)h->L;
+    h->n_rb = (L + 31) / 32;
+    std::vector<int> rb_cam(h->n_rb), rb_split(h->n_rb, 32), lo(cam), hi(cam);
+    for (int rb = 0, v = 0; rb < h->n_rb; ++rb) {
+      while (cam_row_begin[v + 1] <= rb * 32) ++v;
+      rb_cam[rb] = v;
+      const int nxt = cam_row_begin[v + 1];
+      if (v + 1 < cam && nxt < rb * 32 + 32) rb_split[rb] = nxt - rb * 32;
+    }
+    for (int v = 0; v < cam; ++v) {
+      lo[v] = cam_row_begin[v] / 32;
+      hi[v] = (cam_row_begin[v + 1] + 31) / 32;
+    }
+    h->rb_cam = dalloc_t<int>(h, h->n_rb);
+    h->rb_split = dalloc_t<int>(h, h->n_rb);
+    h->cam_rb_lo = dalloc_t<int>(h, cam);
+    h->cam_rb_hi = dalloc_t<int>(h, cam);
+    XC_HIP(hipMemcpy(h->rb_cam, rb_cam.data(), rb_cam.size() * 4, hipMemcpyHostToDevice));
+    XC_HIP(hipMemcpy(h->rb_split, rb_split.data(), rb_split.size() * 4, hipMemcpyHostToDevice));
+    XC_HIP(hipMemcpy(h->cam_rb_lo, lo.data(), lo.size() * 4, hipMemcpyHostToDevice));
+    XC_HIP(hipMemcpy(h->cam_rb_hi, hi.data(), hi.size() * 4, hipMemcpyHostToDevice));
+    h->csum_part = dalloc_t<float>(h, (size_t)2 * h->n_rb * 2 * h->C);
+    h->csum_in = dalloc_t<double>(h, (size_t)h->B * cam * h->C);
+    h->csum_rhat = dalloc_t<double>(h, (size_t)h->S * h->B * cam * h->C);
+  }
 
 }
 
@@ -922,8 +967,22 @@ xc_status xc_forward_chunk(xc_handle* h, int32_t step, float timestep, const flo
         {
           Prof p(h, XC_KERN_GATE);
           const size_t fo = sb * h->fp_rows * h->C;
+          FoldArgs fa{};
+          fa.full = (h->fold && b >= 1) ? 0 : 1;
+          fa.b = b;
+          fa.prev_gateable = b >= 1 && gateable(h, b - 1);
+          fa.flags = h->flags;
+          if (h->fold) {
+            fa.csum_part = h->csum_part;
+            fa.n_rb = h->n_rb;
+            fa.cam_rb_lo = h->cam_rb_lo;
+            fa.cam_rb_hi = h->cam_rb_hi;
+            fa.rb_cam = h->rb_cam;
+            fa.csum_in = h->csum_in;
+            fa.csum_rhat = h->csum_rhat + (size_t)step * h->B * h->n_cams * h->C;
+          }
           launch_fp_compare(x, h->C, h->tables, h->fp + fo, h->fp_alt ? h->fp_alt + fo : nullptr,
-                            h->fp_sel ? h->fp_sel + sb : nullptr, h->fp_records, h->st);
+                            h->fp_sel ? h->fp_sel + sb : nullptr, h->fp_records, fa, h->st);
         }
         {
           Prof p(h, XC_KERN_GATE_DECIDE);
@@ -937,7 +996,7 @@ xc_status xc_forward_chunk(xc_handle* h, int32_t step, float timestep, const flo
           launch_skip_add(h->dtype, x, rhat_tb, out, h->L * h->C, flag, h->st);
         }
       }
-      compute_block(h, b, x, out, flag, rhat_tb, kv_off, Lk);
+      compute_block(h, b, x, out, flag, rhat_tb, kv_off, Lk, false, b + 1 < h->B && gateable(h, b + 1));
       x = out;
     }
     if (h->n >= g.warmup) h->evals_post_warmup += h->B;

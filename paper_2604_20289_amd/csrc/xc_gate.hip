@@ -158,7 +158,8 @@ __device__ void decide(const double* records, int n_wg, const GateArgs& ga, cons
 // the multi-camera shape: 512 threads beat 256 and 1024.)  Every workgroup writes one record per group (zeros for
 // the terms it does not own).
 __global__ __launch_bounds__(kCmpThreads) void fp_compare_kernel(const float* __restrict__ x, int C, FpTables t, float* fp0,
-                                                         float* fp1, const int* sel, double* __restrict__ records) {
+                                                         float* fp1, const int* sel, double* __restrict__ records,
+                                                         FoldArgs fold) {
   // cached fingerprint and where the current one goes
   const bool flip = sel != nullptr && *sel != 0;
   const float* fp_prev = flip ? fp1 : fp0;
@@ -221,39 +222,75 @@ __global__ __launch_bounds__(kCmpThreads) void fp_compare_kernel(const float* __
     const int v = part - n_sp;
     int gv = 0;
     while (gv + 1 < t.n_groups && t.grp_cam_begin[gv + 1] <= v) ++gv;
-    const int cg = threadIdx.x % kColGroups, rl = threadIdx.x / kColGroups;
-    const int c0 = slice * kFpCompareCols + cg * 4;
     const int r0 = t.cam_row_begin[v], r1 = t.cam_row_begin[v + 1];
-    double sx = 0.0, sy = 0.0, sz = 0.0, sw = 0.0;
-    if (c0 < C) {
-      const float* col = x + c0;
-      for (int r = r0 + rl; r < r1; r += kCamUnroll * kCamLanes) {
-        float4 p[kCamUnroll];
+    // this camera's column sums, lane l of the slice's first kFpCompareCols
+    // threads holding column slice * kFpCompareCols + l (fixed-order sums)
+    double tot = 0.0;
+    if (fold.full) {
+      const int cg = threadIdx.x % kColGroups, rl = threadIdx.x / kColGroups;
+      const int c0 = slice * kFpCompareCols + cg * 4;
+      double sx = 0.0, sy = 0.0, sz = 0.0, sw = 0.0;
+      if (c0 < C) {
+        const float* col = x + c0;
+        for (int r = r0 + rl; r < r1; r += kCamUnroll * kCamLanes) {
+          float4 p[kCamUnroll];
 #pragma unroll
-        for (int u = 0; u < kCamUnroll; ++u) {
-          const int rr = r + u * kCamLanes;
-          p[u] = rr < r1 ? *reinterpret_cast<const float4*>(col + (long long)rr * C) : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
+          for (int u = 0; u < kCamUnroll; ++u) {
+            const int rr = r + u * kCamLanes;
+            p[u] = rr < r1 ? *reinterpret_cast<const float4*>(col + (long long)rr * C) : make_float4(0.f, 0.f, 0.f, 0.f);
+          }
 #pragma unroll
-        for (int u = 0; u < kCamUnroll; ++u) {
-          sx += (double)p[u].x;
-          sy += (double)p[u].y;
-          sz += (double)p[u].z;
-          sw += (double)p[u].w;
+          for (int u = 0; u < kCamUnroll; ++u) {
+            sx += (double)p[u].x;
+            sy += (double)p[u].y;
+            sz += (double)p[u].z;
+            sw += (double)p[u].w;
+          }
         }
       }
+      s_cam[cg * 4 + 0][rl] = sx;
+      s_cam[cg * 4 + 1][rl] = sy;
+      s_cam[cg * 4 + 2][rl] = sz;
+      s_cam[cg * 4 + 3][rl] = sw;
+      __syncthreads();
+      if (threadIdx.x < kFpCompareCols)
+        for (int l = 0; l < kCamLanes; ++l) tot += s_cam[threadIdx.x][l];
+    } else {
+      // from block b-1: the partials of its output (computed) or its input
+      // sums plus its stored residual's sums (skipped)
+      const int cl = threadIdx.x % kFpCompareCols, kl = threadIdx.x / kFpCompareCols;
+      constexpr int kLanes = kCmpThreads / kFpCompareCols;
+      const int c = slice * kFpCompareCols + cl;
+      const long long cv = ((long long)(fold.b - 1) * t.n_cams + v) * C + c;
+      if (fold.flags[fold.b - 1] == 0) {
+        const int lo = fold.cam_rb_lo[v], hi = fold.cam_rb_hi[v];
+        const long long kind = (long long)fold.n_rb * 2 * C;
+        double sy = 0.0, sd = 0.0;
+        if (c < C)
+          for (int rb = lo + kl; rb < hi; rb += kLanes) {
+            const long long o = ((long long)rb * 2 + (fold.rb_cam[rb] == v ? 0 : 1)) * C + c;
+            sy += (double)fold.csum_part[o];
+            sd += (double)fold.csum_part[kind + o];
+          }
+        s_cam[cl][kl] = sy;
+        s_cam[cl][kLanes + kl] = sd;
+        __syncthreads();
+        if (threadIdx.x < kFpCompareCols && c < C) {
+          double td = 0.0;
+          for (int l = 0; l < kLanes; ++l) {
+            tot += s_cam[threadIdx.x][l];
+            td += s_cam[threadIdx.x][kLanes + l];
+          }
+          if (fold.prev_gateable) fold.csum_rhat[cv] = td;
+        }
+      } else if (threadIdx.x < kFpCompareCols && c < C) {
+        tot = fold.csum_in[cv] + fold.csum_rhat[cv];
+      }
     }
-    s_cam[cg * 4 + 0][rl] = sx;
-    s_cam[cg * 4 + 1][rl] = sy;
-    s_cam[cg * 4 + 2][rl] = sz;
-    s_cam[cg * 4 + 3][rl] = sw;
-    __syncthreads();
     double acc[3] = {0, 0, 0};
     const int c = slice * kFpCompareCols + threadIdx.x;
     if (threadIdx.x < kFpCompareCols && c < C) {
-      double tot = 0.0;
-#pragma unroll
-      for (int l = 0; l < kCamLanes; ++l) tot += s_cam[threadIdx.x][l];
+      if (fold.csum_in != nullptr) fold.csum_in[((long long)fold.b * t.n_cams + v) * C + c] = tot;
       const float mean = (float)(tot / (double)(r1 - r0));
       const double cur = (double)mean;
       const long long ip = (long long)(t.n_srows + v) * C + c;
@@ -287,9 +324,9 @@ int gate_workgroups(int C, int n_srows, int n_cams) {
 }
 
 void launch_fp_compare(const float* x, int C, const FpTables& t, float* fp0, float* fp1, const int* sel,
-                       double* records, hipStream_t st) {
+                       double* records, const FoldArgs& fold, hipStream_t st) {
   const int grid = gate_workgroups(C, t.n_srows, t.n_cams);
-  fp_compare_kernel<<<grid, kCmpThreads, 0, st>>>(x, C, t, fp0, fp1, sel, records);
+  fp_compare_kernel<<<grid, kCmpThreads, 0, st>>>(x, C, t, fp0, fp1, sel, records, fold);
 }
 
 void launch_gate_decide(const double* records, int n_wg, const GateArgs& ga, const GateState& gs, int sb, int b,

@@ -76,7 +76,11 @@ __device__ __forceinline__ void epilogue(const EpiArgs& e, int m, int n, float a
 // dropped by the hardware), so no branch separates them: the compiler then
 // knows how many stores follow each load batch and waits only for the loads
 // it needs, not for every earlier store.  Loads of rows past M use a clamped
-// row.
+// row.  EPI_DOWN with csum_part: each 32-row block's per-camera column sums of
+// y and of the stored residual (two slots: the camera of the block's first
+// token, the next camera from token rb_split on) are summed in registers
+// over the lane's rows, combined with the partner half-wave and written, one
+// slot per half-wave (a zero-length range when off).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(void* base, long long bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(base, (short)0, (int)bytes, 0x00020000);
 }
@@ -98,6 +102,16 @@ __device__ __forceinline__ void tile_epilogue(const EpiArgs& e, const f32x16 (&a
     gate[nt] = kRes ? e.gate[cb + nt * 32] : 0.f;
   }
   const long long N = e.N;
+  // column-sum partials (EPI_DOWN): per kind one range of n_rb x 2 x N floats
+  const bool csum = kXin && e.csum_part != nullptr;
+  const long long part_bytes = csum ? (long long)e.n_rb * 2 * N * 4 : 0;
+  const __amdgpu_buffer_rsrc_t part_y = tile_rsrc(e.csum_part, part_bytes);
+  const __amdgpu_buffer_rsrc_t part_d = tile_rsrc(e.csum_part + (csum ? (long long)e.n_rb * 2 * N : 0), part_bytes);
+  const int rb0 = (m0 + (r0 & ~31)) >> 5, roff = r0 & 31;  // the lane's first 32-row block, its offset in it
+  int split[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) split[mt] = csum ? e.rb_split[min(rb0 + mt, e.n_rb - 1)] : 32;
+  float sy[2][NT], sd[2][NT];
   float res[2][4][NT], xin[2][4][NT];
   auto load = [&](int blk, int slot) __attribute__((always_inline)) {
     const int mt = blk >> 2, g = blk & 3;
@@ -148,6 +162,41 @@ __device__ __forceinline__ void tile_epilogue(const EpiArgs& e, const f32x16 (&a
           const bf16 d = (bf16)(y - xin[slot][r][nt]);
           // out_t == null: a zero-length range drops the cached-residual store
           __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, d), out_b, o * 2, 0, 0);
+          // column sums: rows past M count nowhere; the slot follows the camera boundary
+          const int ro = roff + g * 8 + r;
+          const float w = m0 + r0 + mt * 32 + g * 8 + r < M ? 1.f : 0.f;
+          const float w1 = ro >= split[mt] ? w : 0.f, w0 = w - w1;
+          if (g == 0 && r == 0) {
+            sy[0][nt] = w0 * y;
+            sy[1][nt] = w1 * y;
+            sd[0][nt] = w0 * (float)d;
+            sd[1][nt] = w1 * (float)d;
+          } else {
+            sy[0][nt] = fmaf(w0, y, sy[0][nt]);
+            sy[1][nt] = fmaf(w1, y, sy[1][nt]);
+            sd[0][nt] = fmaf(w0, (float)d, sd[0][nt]);
+            sd[1][nt] = fmaf(w1, (float)d, sd[1][nt]);
+          }
+        }
+      }
+    }
+    if constexpr (kXin) {
+      if (g == 3) {
+        // this 32-row block is complete: add the partner half-wave (the other
+        // 16 rows), then half-wave hi writes slot hi
+        const int hi = (r0 >> 2) & 1;
+        const int rbo = ((rb0 + mt) * 2 + hi) * (int)N;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          float t[4] = {sy[0][nt], sy[1][nt], sd[0][nt], sd[1][nt]};
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(t[k]), __float_as_uint(t[k]), false, false);
+            t[k] = __uint_as_float(pr[0]) + __uint_as_float(pr[1]);
+          }
+          const int o = (rbo + cb + nt * 32) * 4;
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, hi ? t[1] : t[0]), part_y, o, 0, 0);
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, hi ? t[3] : t[2]), part_d, o, 0, 0);
         }
       }
     }

@@ -63,12 +63,42 @@ struct EpiArgs {
   // of (q, k, v): part_base 0 for the [q; k; v] projection, 1 for [k; v]
   int part_base;
   RopeArgs rope;       // rotation of q and k (tab == null: none)
+  // EPI_DOWN, optional (null: off): per-camera column-sum partials of the
+  // block output y and of the stored residual (the bf16 values), one pair of
+  // rows per 32-row block of tokens: csum_part[kind][rb][slot][N], kind 0 = y,
+  // 1 = residual, slot 0 = the camera of the block's first token, slot 1 = the
+  // next camera, which starts at token offset rb_split[rb] (32: none)
+  float* csum_part;
+  const int* rb_split;
+  int n_rb;
   const float* gq;     // [D]
   const float* gk;     // [D]
   void* q_out;         // [H][Mpad][D]
   void* k_cache;       // [H][Lcap][D], token m at row kv_off + m
   void* vt_cache;      // [H][D][Lcap], token m at column kv_off + m
   int H, D, Mpad, Lcap, kv_off;
+};
+
+// Global-channel sources of a gated evaluation (the column sums of the block
+// input per camera), so that the comparison kernel need not read every token:
+//   mode FULL: read x;
+//   otherwise block b-1's skip flag selects: computed -> sum the 32-row-block
+//   partials its MLP-down epilogue wrote (and, for a gateable b-1, refresh the
+//   sums of its stored residual, csum_rhat[b-1]); skipped -> the input sums of
+//   b-1 plus the sums of its stored residual (x_b = x_{b-1} + r_hat).
+// Every evaluation leaves its input's sums in csum_in[b] for block b+1.
+struct FoldArgs {
+  int full;                  // 1: read x (no partials for this block)
+  int b;
+  int prev_gateable;
+  const int* flags;          // [B] skip flags of this pass
+  const float* csum_part;    // see EpiArgs
+  int n_rb;
+  const int* cam_rb_lo;      // [n_cams] first 32-row block holding a token of the camera
+  const int* cam_rb_hi;      // [n_cams] one past the last such block
+  const int* rb_cam;         // [n_rb] camera of each block's first token
+  double* csum_in;           // [B][n_cams][C] this pass's input sums of each gated block (null: none kept)
+  double* csum_rhat;         // [B][n_cams][C] residual sums of step t
 };
 
 // Per-pass gate hyper-parameters handed to the decision kernel.
@@ -149,7 +179,7 @@ void launch_pass_begin(const GateState& gs, int n_blocks, hipStream_t st);
 // gate_workgroups(...) * kMaxGroups * kFpRecord doubles.
 int gate_workgroups(int C, int n_srows, int n_cams);
 void launch_fp_compare(const float* x, int C, const FpTables& t, float* fp0, float* fp1, const int* sel,
-                       double* records, hipStream_t st);
+                       double* records, const FoldArgs& fold, hipStream_t st);
 // Second launch: the decision from the records of the first.
 void launch_gate_decide(const double* records, int n_wg, const GateArgs& ga, const GateState& gs, int sb, int b,
                         int evaluate, hipStream_t st);

@@ -363,3 +363,16 @@ def test_condition_required_and_validated():
         assert e.value.status == xcp.XC_ERR_STATE
     finally:
         plain.close()
+
+
+def test_bf16_small_cameras_read_the_block_input():
+    """Cameras of 25 tokens (fewer than the 32-token blocks of the MLP-down
+    column-sum partials): the gate reads the camera means from the block input
+    itself; 12 cameras in one view group, natural skips."""
+    w = synth.with_model(BF_RAGGED, groups=(synth.ViewGroup(12, 1, 5, 5),))
+    ls = _ls(w)
+    try:
+        st = ls.run(5, tol_rel_l2=TOLBF)
+        print(f"[parity] bf16-small-cameras skips={st['skips']} band={ls.band_hits}", flush=True)
+    finally:
+        ls.close()
