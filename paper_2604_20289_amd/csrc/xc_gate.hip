@@ -84,29 +84,41 @@ __device__ void decide(const double* records, int n_wg, const GateArgs& ga, cons
     }
     return;
   }
+  // the per-(t, b) state the tail needs, fetched now so its latency overlaps
+  // the record reduction (the records were written on every XCD: each load
+  // round trip goes past this XCD's L2)
+  float ema0 = 0.f;
+  int stale0 = 0;
+  if (lane == 0) {
+    ema0 = gs.ema[sb];
+    stale0 = gs.stale[sb];
+  }
   double s_min = 1e300, d_max = -1e300;
   for (int g = 0; g < ga.n_groups; ++g) {
-    // threads stride the workgroup records (one 64-byte record per load
-    // batch, two batches in flight); fixed-shape reductions keep the sums
-    // deterministic
+    // threads stride the workgroup records (64 bytes each), up to kBatch
+    // records per thread loaded in one round; fixed-shape reductions keep
+    // the sums deterministic
+    constexpr int kBatch = 4;
     double tot[kRec] = {0, 0, 0, 0, 0, 0, 0, 0};
-    auto add = [&](int w) __attribute__((always_inline)) {
-      const double2* r2 = reinterpret_cast<const double2*>(records + ((long long)w * kMaxGroups + g) * kRec);
-      double2 d[kRec / 2];
+    for (int w0 = 0; w0 < n_wg; w0 += 256 * kBatch) {
+      double2 d[kBatch][kRec / 2];
 #pragma unroll
-      for (int k = 0; k < kRec / 2; ++k) d[k] = r2[k];
+      for (int u = 0; u < kBatch; ++u) {
+        const int w = w0 + u * 256 + (int)threadIdx.x;
+        const double2* r2 = reinterpret_cast<const double2*>(records + ((long long)min(w, n_wg - 1) * kMaxGroups + g) * kRec);
 #pragma unroll
-      for (int k = 0; k < kRec / 2; ++k) {
-        tot[2 * k] = (2 * k == 3) ? fmax(tot[2 * k], d[k].x) : tot[2 * k] + d[k].x;
-        tot[2 * k + 1] = (2 * k + 1 == 3) ? fmax(tot[2 * k + 1], d[k].y) : tot[2 * k + 1] + d[k].y;
+        for (int k = 0; k < kRec / 2; ++k) d[u][k] = r2[k];
       }
-    };
-    int w = threadIdx.x;
-    for (; w + 256 < n_wg; w += 512) {
-      add(w);
-      add(w + 256);
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        if (w0 + u * 256 + (int)threadIdx.x >= n_wg) continue;
+#pragma unroll
+        for (int k = 0; k < kRec / 2; ++k) {
+          tot[2 * k] = (2 * k == 3) ? fmax(tot[2 * k], d[u][k].x) : tot[2 * k] + d[u][k].x;
+          tot[2 * k + 1] = (2 * k + 1 == 3) ? fmax(tot[2 * k + 1], d[u][k].y) : tot[2 * k + 1] + d[u][k].y;
+        }
+      }
     }
-    if (w < n_wg) add(w);
     block_reduce_n<kRec>(tot, s_red, 3);
     double cs = cos_from(tot[0], tot[1], tot[2]);
     double cg = cos_from(tot[5], tot[6], tot[7]);
@@ -126,7 +138,7 @@ __device__ void decide(const double* records, int n_wg, const GateArgs& ga, cons
     s_min = fmin(s_min, cos_from(dot, nn, pp));
   }
   if (lane != 0) return;
-  double ema = (double)gs.ema[sb];
+  double ema = (double)ema0;
   const bool has_ema = !isnan(ema);
   double tau;
   if (ga.adaptive)
@@ -138,7 +150,7 @@ __device__ void decide(const double* records, int n_wg, const GateArgs& ga, cons
     double e = has_ema ? (double)ga.alpha * s_min + (1.0 - (double)ga.alpha) * ema : s_min;
     gs.ema[sb] = (float)e;
   }
-  const int stale = gs.stale[sb];
+  const int stale = stale0;
   const bool skip = (s_min >= tau) && (d_max < (double)ga.tau_dev) && (ga.max_stale == 0 || stale < ga.max_stale);
   gs.flags[b] = skip ? 1 : 0;
   gs.stale[sb] = skip ? stale + 1 : 0;
