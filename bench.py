@@ -13,10 +13,10 @@ Runs, in order:
   1. gate on, `warmup` untimed chunks then `steps` timed chunks -> mean
      chunk latency (the reported value; the paper reports the average
      per-chunk DiT time) and block skip rate;
-  2. gate off (every block computed, same kernels), same chunks, with HIP
-     events around every kernel launch -> full-compute latency, effective
-     block TFLOP/s, per-kernel durations and the roofline of the dominant
-     kernel (attention);
+  2. gate off (every block computed, same kernels), same chunks ->
+     full-compute latency and effective block TFLOP/s; then the same chunks
+     again with HIP events around every kernel launch -> per-kernel
+     durations and the roofline of the dominant kernel (attention);
   3. gate on again for two chunks with kernel events -> gate-kernel GB/s;
   4. the CPU oracle on a bounded sample (one computed block at the full
      shape, float64 numpy on the host cores), scaled to ms per chunk.
@@ -321,11 +321,15 @@ def main():
                    "mean_ms_after_warmup": round(statistics.mean(cad_ms[args.warmup:]), 3)}
         log(f"force every {args.force_every}: skip fractions {cadence['chunk_skip_fraction']}")
 
-    # 2. gate off
+    # 2. gate off: the chunk latency without kernel events, then the same
+    # chunks again with an event pair around every launch for the kernel table
+    # (the events cost a few microseconds per launch: visible on small models)
     off_ms, kt = None, {}
     if not args.no_gate_off:
         xc = make_xc(synth.with_gate(w, enabled=0).gate)
-        off_ms = [v[0] for v in run_stream(xc, m, eps_dev, actions, args.warmup, args.steps, torch, profile=True)]
+        off_ms = [v[0] for v in run_stream(xc, m, eps_dev, actions, args.warmup, args.steps, torch)]
+        xc.reset()
+        run_stream(xc, m, eps_dev, actions, args.warmup, args.steps, torch, profile=True)
         kt = kernel_table(xc, xcp)
         xc.close()
         log(f"gate off: mean {statistics.mean(off_ms):.2f} ms/chunk")
