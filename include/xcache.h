@@ -195,7 +195,12 @@ xc_status xc_init(const xc_model_config* model, const xc_gate_config* gate,
  * The current chunk's keys/values of each computed block are written into
  * this generation's cache slot and attended together with the kept past
  * chunks; they are replaced by the clean ones at xc_kv_update.
- * Decisions stay on the device; nothing is copied back. */
+ * Decisions stay on the device; nothing is copied back.
+ * Errors (nothing is enqueued and no state changes): XC_ERR_INVALID_ARG
+ * (NULL pointer, step out of range, unknown flag, non-finite timestep or
+ * action), XC_ERR_STATE (the action differs bitwise from the one this
+ * generation's first pass used: one chunk has one action, Section 2.3.2; or
+ * a cross-attention model has no condition yet), XC_ERR_HIP (sticky). */
 xc_status xc_forward_chunk(xc_handle* h, int32_t step, float timestep, const float* action_host,
                            const void* x_in, void* x_out, uint32_t flags);
 
@@ -207,7 +212,10 @@ xc_status xc_forward_chunk(xc_handle* h, int32_t step, float timestep, const flo
  *   x_clean : device float32 [L, C].
  *   x_out   : device float32 [L, C], or NULL when the pass's output is not
  *             needed: the last block then stops after its key/value
- *             projection (its attention and MLP feed nothing else). */
+ *             projection (its attention and MLP feed nothing else).
+ * Errors as xc_forward_chunk: the action must be the one this generation's
+ * denoising passes used (XC_ERR_STATE otherwise); xc_reset and a completed
+ * xc_kv_update release it. */
 xc_status xc_kv_update(xc_handle* h, float timestep, const float* action_host,
                        const void* x_clean, void* x_out);
 

@@ -105,6 +105,10 @@ struct xc_handle {
   bool any_forward = false;
   float action_prev[kMaxAction] = {};
   bool have_action_prev = false;
+  // the action of the current generation, fixed by its first pass: every
+  // pass of one chunk (denoising steps and the clean pass) conditions on it
+  float action_cur[kMaxAction] = {};
+  bool have_action_cur = false;
   bool sticky = false;
   // profiling
   bool profiling = false;
@@ -117,6 +121,17 @@ namespace {
 
 bool gateable(const xc_handle* h, int b) {
   return h->g.enabled && b >= h->g.front_anchors && b < h->B - h->g.back_anchors;
+}
+
+// an action that differs from the one this generation's first pass fixed
+bool action_changed(const xc_handle* h, const float* a) {
+  return h->have_action_cur && std::memcmp(h->action_cur, a, sizeof(float) * (size_t)h->A) != 0;
+}
+
+void fix_action(xc_handle* h, const float* a) {
+  if (h->have_action_cur) return;
+  std::memcpy(h->action_cur, a, sizeof(float) * (size_t)h->A);
+  h->have_action_cur = true;
 }
 
 long long tokens_of(const xc_model_config* m) {
@@ -688,6 +703,7 @@ void reset_state(xc_handle* h) {
   h->last_step = -1;
   h->any_forward = false;
   h->have_action_prev = false;
+  h->have_action_cur = false;
 }
 
 void free_all(xc_handle* h) {
@@ -944,8 +960,10 @@ xc_status xc_forward_chunk(xc_handle* h, int32_t step, float timestep, const flo
   if (!std::isfinite(timestep)) return XC_ERR_INVALID_ARG;
   for (int i = 0; i < h->A; ++i)
     if (!std::isfinite(action_host[i])) return XC_ERR_INVALID_ARG;
+  if (action_changed(h, action_host)) return XC_ERR_STATE;
   try {
     XC_HIP(hipSetDevice(h->device));
+    fix_action(h, action_host);
     const xc_gate_config& g = h->g;
     const bool forced_all = !g.enabled || h->n < g.warmup || (flags & XC_FORCE_FULL) ||
                             (step == 0 && g.step0_mode == XC_STEP0_FORCE);
@@ -1017,6 +1035,7 @@ xc_status xc_kv_update(xc_handle* h, float timestep, const float* action_host, c
   if (!std::isfinite(timestep)) return XC_ERR_INVALID_ARG;
   for (int i = 0; i < h->A; ++i)
     if (!std::isfinite(action_host[i])) return XC_ERR_INVALID_ARG;
+  if (action_changed(h, action_host)) return XC_ERR_STATE;
   try {
     XC_HIP(hipSetDevice(h->device));
     pass_conditioning(h, timestep, action_host);
@@ -1032,6 +1051,7 @@ xc_status xc_kv_update(xc_handle* h, float timestep, const float* action_host, c
     h->kv_block_evals += h->B;
     for (int i = 0; i < h->A; ++i) h->action_prev[i] = action_host[i];
     h->have_action_prev = true;
+    h->have_action_cur = false;
     h->n += 1;
     refresh_rope(h);
     h->last_step = h->S;

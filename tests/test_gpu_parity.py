@@ -365,6 +365,42 @@ def test_condition_required_and_validated():
         plain.close()
 
 
+def test_action_fixed_per_generation():
+    """One chunk has one action (the condition channel changes once per
+    generation, Section 2.3.2): a pass of the same generation with another
+    action is refused with no state change; the clean pass releases it."""
+    _need_gpu()
+    from paper_2604_20289_amd import xcache as xcp
+    w = W0
+    dev = torch.device("cuda")
+    xc = xcp.XCache(w.model, w.gate, synth.make_weights(w.model), torch.cuda.current_stream().cuda_stream)
+    try:
+        x = torch.randn((w.model.tokens, w.model.hidden), dtype=torch.float32, device=dev)
+        y = torch.empty_like(x)
+        a0 = np.zeros(w.model.action_dim, np.float32)
+        a1 = a0.copy()
+        a1[0] = 0.5
+        xc.forward_chunk(0, 900.0, a0, x, y)
+        before = xc.stats()
+        for call in (lambda: xc.forward_chunk(1, 800.0, a1, x, y),
+                     lambda: xc.kv_update(synth.KV_UPDATE_TIMESTEP, a1, x, None)):
+            with pytest.raises(xcp.XCacheError) as e:
+                call()
+            assert e.value.status == xcp.XC_ERR_STATE
+        after = xc.stats()
+        assert (after["last_step"], after["generations"], after["kv_block_evals"]) == \
+            (before["last_step"], before["generations"], before["kv_block_evals"])
+        xc.forward_chunk(1, 800.0, a0, x, y)
+        xc.kv_update(synth.KV_UPDATE_TIMESTEP, a0, x, None)
+        xc.forward_chunk(0, 900.0, a1, x, y)        # the next generation takes a new action
+        xc.reset()
+        xc.forward_chunk(0, 900.0, a0, x, y)        # and so does a reset rollout
+        torch.cuda.synchronize()
+        assert xc.stats()["generations"] == 0
+    finally:
+        xc.close()
+
+
 def test_bf16_small_cameras_read_the_block_input():
     """Cameras of 25 tokens (fewer than the 32-token blocks of the MLP-down
     column-sum partials): the gate reads the camera means from the block input
