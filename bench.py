@@ -432,8 +432,9 @@ def main():
                 (4.0 * L * C + 8.0 * fp_rows * C)
             e["gbs"] = round(e["bytes"] / (v["avg_us"] * 1e-6) / 1e9, 1)
             e["hbm_frac"] = round(e["gbs"] / PEAK_HBM_GBS, 4)
-        if k == "skip_add":
-            e["note"] = "averaged over launches that add and launches that return at entry"
+        if k == "ln_mod":
+            e["note"] = ("the first LayerNorm launch of a gated evaluation writes x + r_hat when the block "
+                         "is skipped: averaged over LayerNorm, skip-path and return-at-entry launches")
         gk[k] = e
     res["kernels_gate_on"] = gk
     if not args.no_cpu_baseline:

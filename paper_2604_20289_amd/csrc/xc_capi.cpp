@@ -450,8 +450,10 @@ void compute_block(xc_handle* h, int b, const float* x, float* out, const int* f
   void* kc_b = wptr<void>(h->kc, (size_t)b * H * h->Lcap * D, esz);
   void* vt_b = wptr<void>(h->vt, (size_t)b * H * h->Lcap * D, esz);
   {
+    // a skipped block's output x + rhat is written by this launch (Eq. 4)
     Prof p(h, XC_KERN_LN_MOD);
-    launch_ln_mod(h->dtype, x, shift1, scale1, h->hbuf, L, C, flag, h->st);
+    launch_ln_mod(h->dtype, x, shift1, scale1, h->hbuf, L, C, flag, h->st, flag ? rhat_tb : nullptr,
+                  flag ? out : nullptr);
   }
   if (h->dtype == XC_BF16) {
     // QKV projection with the per-head RMSNorm and the cache writes fused
@@ -1009,9 +1011,7 @@ xc_status xc_forward_chunk(xc_handle* h, int32_t step, float timestep, const flo
         h->visited[sb] = 1;
         if (evaluate) {
           ++h->gated_evals;
-          flag = h->flags + b;
-          Prof p(h, XC_KERN_SKIP_ADD);
-          launch_skip_add(h->dtype, x, rhat_tb, out, h->L * h->C, flag, h->st);
+          flag = h->flags + b;  // the block's first LayerNorm kernel also runs the skip path
         }
       }
       compute_block(h, b, x, out, flag, rhat_tb, kv_off, Lk, false, b + 1 < h->B && gateable(h, b + 1));

@@ -121,16 +121,37 @@ __global__ __launch_bounds__(256) void adaln_kernel(const T* __restrict__ w, con
 
 // h = LayerNorm(x) * (1 + scale) + shift per row (no affine, biased variance,
 // eps 1e-6), one wave per row, values held in registers between the passes.
+// With a skip flag that is set the block is skipped: the kernel then writes
+// the skip path's output skip_out = x + rhat (Eq. 4) for its rows instead
+// when skip_out is given (the first LayerNorm of a gated block evaluation),
+// else returns at entry.  skip_out may alias x (element-wise, in place).
 template <typename T, int MAXV>
-__global__ __launch_bounds__(256) void ln_mod_kernel(const float* __restrict__ x, const float* __restrict__ shift,
+__global__ __launch_bounds__(256) void ln_mod_kernel(const float* x, const float* __restrict__ shift,
                                                      const float* __restrict__ scale, T* __restrict__ out, int L,
-                                                     int C, const int* __restrict__ flag) {
-  if (flag != nullptr && *flag) return;
+                                                     int C, const int* __restrict__ flag,
+                                                     const T* __restrict__ rhat, float* skip_out) {
+  const bool skip = flag != nullptr && *flag;
+  if (skip && skip_out == nullptr) return;
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= L) return;
   const int C4 = C >> 2;
   const float4* xr = reinterpret_cast<const float4*>(x + (long long)row * C);
+  if (skip) {
+    typedef T T4 __attribute__((ext_vector_type(4)));
+    const T4* rr = reinterpret_cast<const T4*>(rhat + (long long)row * C);
+    float4* orow = reinterpret_cast<float4*>(skip_out + (long long)row * C);
+#pragma unroll
+    for (int i = 0; i < MAXV; ++i) {
+      const int c4 = lane + i * 64;
+      if (c4 < C4) {
+        const float4 a = xr[c4];
+        const T4 r = rr[c4];
+        orow[c4] = make_float4(a.x + to_f(r[0]), a.y + to_f(r[1]), a.z + to_f(r[2]), a.w + to_f(r[3]));
+      }
+    }
+    return;
+  }
   float4 v[MAXV];
   float s = 0.f;
 #pragma unroll
@@ -271,24 +292,6 @@ __global__ void rope_table_kernel(float2* __restrict__ tab, RopeArgs r, int n_sl
   }
 }
 
-// Skipped block (Eq. 4): out = x + rhat; runs only when the skip flag is set.
-template <typename T>
-__global__ __launch_bounds__(256) void skip_add_kernel(const float* __restrict__ x, const T* __restrict__ rhat,
-                                                       float* __restrict__ out, long long n4,
-                                                       const int* __restrict__ flag) {
-  if (*flag == 0) return;
-  for (long long i = blockIdx.x * 256ll + threadIdx.x; i < n4; i += (long long)gridDim.x * 256) {
-    float4 a = reinterpret_cast<const float4*>(x)[i];
-    const T* r = rhat + i * 4;
-    float4 o;
-    o.x = a.x + to_f(r[0]);
-    o.y = a.y + to_f(r[1]);
-    o.z = a.z + to_f(r[2]);
-    o.w = a.w + to_f(r[3]);
-    reinterpret_cast<float4*>(out)[i] = o;
-  }
-}
-
 __global__ void axpby_kernel(float a, const float* __restrict__ x, float b, const float* __restrict__ y,
                              float* __restrict__ out, long long n) {
   for (long long i = blockIdx.x * 256ll + threadIdx.x; i < n; i += (long long)gridDim.x * 256)
@@ -340,10 +343,11 @@ void launch_adaln(int dtype, const void* w_ada, const float* b_ada, const float*
 }
 
 void launch_ln_mod(int dtype, const float* x, const float* shift, const float* scale, void* out, int L, int C,
-                   const int* flag, hipStream_t st) {
+                   const int* flag, hipStream_t st, const void* rhat, float* skip_out) {
   int grid = (L + 3) / 4;
   int maxv = (C / 4 + 63) / 64;
-#define XC_LN(T, MV) ln_mod_kernel<T, MV><<<grid, 256, 0, st>>>(x, shift, scale, (T*)out, L, C, flag)
+#define XC_LN(T, MV) \
+  ln_mod_kernel<T, MV><<<grid, 256, 0, st>>>(x, shift, scale, (T*)out, L, C, flag, (const T*)rhat, skip_out)
   if (dtype == 1) {
     if (maxv <= 2) XC_LN(bf16, 2);
     else if (maxv <= 8) XC_LN(bf16, 8);
@@ -373,16 +377,6 @@ void launch_rope_table(float2* tab, const RopeArgs& r, int n_slots, const int* s
   const int total = n_slots * r.np[0] + rows * r.np[1] + cols * r.np[2];
   rope_table_kernel<<<(total + 255) / 256, 256, 0, st>>>(tab, r, n_slots, slot_frames, slot_frame, rows, cols,
                                                          log(theta), n);
-}
-
-void launch_skip_add(int dtype, const float* x, const void* rhat, float* out, long long n, const int* flag,
-                     hipStream_t st) {
-  long long n4 = n / 4;
-  int grid = grid_for(n4, 256 * 4);
-  if (dtype == 1)
-    skip_add_kernel<bf16><<<grid, 256, 0, st>>>(x, (const bf16*)rhat, out, n4, flag);
-  else
-    skip_add_kernel<float><<<grid, 256, 0, st>>>(x, (const float*)rhat, out, n4, flag);
 }
 
 void launch_axpby(float a, const float* x, float b, const float* y, float* out, long long n, hipStream_t st) {

@@ -145,8 +145,10 @@ void launch_cond(const float* action, int temb_dim, int action_dim, float timest
                  hipStream_t st);
 void launch_adaln(int dtype, const void* w_ada, const float* b_ada, const float* cond_silu, int rows_per_block,
                   long long block_stride_w, int n_blocks, int dc, float* mod, hipStream_t st);
+// rhat / skip_out: when the skip flag is set, write skip_out = x + rhat
+// (the skip path) instead of returning at entry
 void launch_ln_mod(int dtype, const float* x, const float* shift, const float* scale, void* out, int L, int C,
-                   const int* flag, hipStream_t st);
+                   const int* flag, hipStream_t st, const void* rhat = nullptr, float* skip_out = nullptr);
 void launch_gemm(int dtype, EpiMode mode, const void* A, const void* W, int M, int N, int K, const EpiArgs& e,
                  const int* flag, hipStream_t st);
 // float32 models: per-head RMSNorm * gain of q and k (with the rotary
@@ -168,8 +170,6 @@ void launch_rope_table(float2* tab, const RopeArgs& r, int n_slots, const int* s
 size_t attention_workspace_floats(int L, int Lk, int H, int D);
 void launch_attention(int dtype, const void* q, const void* kring, const void* vtring, void* o, float* ws, int L,
                       int Mpad, int Lcap, int Lk, int H, int D, const int* flag, hipStream_t st);
-void launch_skip_add(int dtype, const float* x, const void* rhat, float* out, long long n, const int* flag,
-                     hipStream_t st);
 void launch_axpby(float a, const float* x, float b, const float* y, float* out, long long n, hipStream_t st);
 void launch_pass_begin(const GateState& gs, int n_blocks, hipStream_t st);
 // Gated evaluation, first launch: fingerprint of x against the (t, b) cache
