@@ -147,3 +147,15 @@ def test_fingerprint_rows_match_oracle(model, gate):
     want = np.concatenate([r.reshape(-1) for r in xo.fingerprint_rows(model.groups, gate.fp_budget, gate.fp_mode)])
     got = xcp.xc_fingerprint_rows(model, gate)
     np.testing.assert_array_equal(got, want)
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py measures one GPU; --gpus N > 1 exits with a message before any device work."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120, cwd=root)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout.strip() == ""
