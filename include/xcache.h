@@ -83,7 +83,9 @@ typedef struct xc_view_group {
  * Constraints: hidden == n_heads * head_dim; temb_dim even;
  * temb_dim + action_dim <= XC_MAX_COND; action_dim <= XC_MAX_ACTION;
  * XC_BF16 additionally needs head_dim in {64, 128} and hidden, mlp_hidden
- * multiples of 128.  Block internals: LayerNorm without affine (eps 1e-6),
+ * multiples of 128.  Size limits of this build (32-bit kernel offsets;
+ * XC_ERR_UNSUPPORTED beyond them): kv_window * L <= 2^24 keys and
+ * ceil(L / 32) * 2 * hidden * 4 < 2^31.  Block internals: LayerNorm without affine (eps 1e-6),
  * six-way adaLN modulation from W_ada SiLU(c) + b_ada with
  * c = [sinusoidal temb(timestep); action], QK RMSNorm (eps 1e-6) with gains,
  * softmax attention over the rolling cache (no mask), tanh-GELU MLP.
@@ -175,7 +177,8 @@ const char* xc_status_string(xc_status s);
  *   hip_stream      : hipStream_t all work is enqueued on (NULL = default).
  *   out             : receives the handle.
  * Errors: XC_ERR_INVALID_ARG (NULL pointers, bad shape or gate field, size
- * mismatch), XC_ERR_UNSUPPORTED (kv_protect == 0, unsupported head_dim),
+ * mismatch), XC_ERR_UNSUPPORTED (kv_protect == 0, unsupported head_dim,
+ * a shape past the size limits above),
  * XC_ERR_OOM, XC_ERR_HIP.  Synchronises the stream once (weight upload). */
 xc_status xc_init(const xc_model_config* model, const xc_gate_config* gate,
                   const float* weights_host, size_t weights_bytes, void* hip_stream,

@@ -119,6 +119,11 @@ struct xc_handle {
 
 namespace {
 
+// largest visible key window (W_kv x L) and largest per-kind column-sum
+// partial buffer (bytes) whose kernel offsets fit in 32 bits
+constexpr long long kMaxWindowKeys = 1ll << 24;
+constexpr long long kMaxPartialBytes = (1ll << 31) - 1;
+
 bool gateable(const xc_handle* h, int b) {
   return h->g.enabled && b >= h->g.front_anchors && b < h->B - h->g.back_anchors;
 }
@@ -165,6 +170,11 @@ xc_status validate_model(const xc_model_config* m) {
   const long long L = tokens_of(m);
   if (L < 1 || L > (1ll << 24)) return XC_ERR_INVALID_ARG;
   if ((long long)m->kv_window * L > (1ll << 28)) return XC_ERR_INVALID_ARG;
+  // shapes whose 32-bit kernel offsets would wrap: the attention kernel's
+  // per-thread V^T staging offset spans up to 63 rows of Lcap keys (bf16),
+  // the MLP-down epilogue's column-sum partials ceil(L/32) x 2 x C floats
+  if ((long long)m->kv_window * L > kMaxWindowKeys) return XC_ERR_UNSUPPORTED;
+  if ((L + 31) / 32 * 2 * (long long)m->hidden * 4 > kMaxPartialBytes) return XC_ERR_UNSUPPORTED;
   if (m->dtype == XC_BF16) {
     if (m->head_dim != 64 && m->head_dim != 128) return XC_ERR_UNSUPPORTED;
     if (m->hidden % 128 != 0 || m->mlp_hidden % 128 != 0) return XC_ERR_UNSUPPORTED;

@@ -76,6 +76,30 @@ def test_init_rejects_bad_model(change, want):
     assert _init_status(m, W0.gate, weights) == want
 
 
+@pytest.mark.parametrize("change", [
+    # 4 x 4,198,400 = 16,793,600 visible keys > 2^24: the attention kernel's V^T staging offset would wrap
+    dict(kv_window=4, groups=(synth.ViewGroup(4, 1, 1024, 1025),)),
+    # hidden 4096, L = 2^21: ceil(L/32) * 2 * C * 4 = 2^31 bytes of column-sum partials per kind
+    dict(n_heads=32, head_dim=128, hidden=4096, kv_window=1, groups=(synth.ViewGroup(1, 1, 2048, 1024),)),
+    dict(n_heads=32, head_dim=128, hidden=4096, kv_window=1, dtype="bf16",
+         groups=(synth.ViewGroup(2, 1, 1024, 1024),)),
+])
+def test_init_rejects_shapes_past_32bit_offsets(change):
+    """Shapes whose kernel offsets would not fit in 32 bits are refused before
+    anything is allocated (the weight blob is not even looked at)."""
+    m = synth.with_model(W0, **change).model
+    assert _init_status(m, W0.gate, np.zeros(1, np.float32)) == xcp.XC_ERR_UNSUPPORTED
+    # one fewer camera row / window chunk is inside the limits: validation then reaches the size check
+    smaller = dict(change)
+    if change["kv_window"] > 1:
+        smaller["kv_window"] = 3
+    else:
+        g = change["groups"][0]
+        smaller["groups"] = (synth.ViewGroup(g.views, g.frames, g.height - 1, g.width),)
+    m2 = synth.with_model(W0, **smaller).model
+    assert _init_status(m2, W0.gate, np.zeros(1, np.float32)) == xcp.XC_ERR_INVALID_ARG
+
+
 @pytest.mark.parametrize("change,want", [
     (dict(kv_protect=0), xcp.XC_ERR_UNSUPPORTED),
     (dict(kv_protect=2), xcp.XC_ERR_INVALID_ARG),
