@@ -207,6 +207,31 @@ xc_status xc_init(const xc_model_config* model, const xc_gate_config* gate,
 xc_status xc_forward_chunk(xc_handle* h, int32_t step, float timestep, const float* action_host,
                            const void* x_in, void* x_out, uint32_t flags);
 
+/* Bytes of the static device array that xc_forward_chunk_noalloc uses as its
+ * scratch (one copy per GPU the library runs on, held until the process
+ * ends). */
+#define XC_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* xc_forward_chunk for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same pass with the same arguments, state and errors, but the kernels'
+ * per-pass scratch -- the gate's per-workgroup partial records and the
+ * attention's key-split partials -- lives in a static device array of
+ * XC_NOALLOC_SCRATCH_BYTES instead of the handle's buffers.  The call
+ * allocates nothing (no hipMalloc, no events: xc_profile records none of its
+ * launches).  The attention splits its keys over workgroups only as far as
+ * the partials fit in what the records leave of the array (possibly not at
+ * all), so its output may differ from xc_forward_chunk's by rounding.
+ * Every handle on one GPU shares that GPU's array, and the array keeps the
+ * last call's contents (each pass writes every value it reads): passes of
+ * this entry point that overlap on one GPU (different handles on streams
+ * that run concurrently) race.  Errors as xc_forward_chunk, plus
+ * XC_ERR_UNSUPPORTED when the gate's records alone exceed the array and
+ * XC_ERR_STATE when the array's device address could not be obtained at
+ * xc_init. */
+xc_status xc_forward_chunk_noalloc(xc_handle* h, int32_t step, float timestep, const float* action_host,
+                                   const void* x_in, void* x_out, uint32_t flags);
+
 /* The KV-update pass (Section 2.1; protection of Section 2.5 item 3): every
  * block computed in full on the clean latent, its keys/values committed to
  * the generation's slot of the rolling cache (the oldest chunk is evicted once

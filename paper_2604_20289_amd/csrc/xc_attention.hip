@@ -482,14 +482,16 @@ int resident_attention_groups() {
 // workgroup: rounds * (tiles per unit + 4 for the unit's prologue and
 // epilogue) + 4 S items / (resident workgroups) for the merge, over S <= 4
 // with chunks of at least 4 tiles (fitted to measured split sweeps on the
-// multi-camera shapes).
-int attention_splits(int L, int Lk, int H) {
+// multi-camera shapes); only split counts whose partials fit in cap_floats
+// workspace floats are considered (S = 1 needs none).
+int attention_splits(int L, int Lk, int H, int D, size_t cap_floats) {
   const int items = H * ((L + kQT - 1) / kQT);
   const int NT = (Lk + 63) / 64;
   const int slots = resident_attention_groups();
   int best = 1;
   double best_cost = 1e300;
   for (int s = 1; s <= 4 && (s == 1 || NT / s >= 4); ++s) {
+    if (s > 1 && (size_t)items * s * (size_t)piece_floats(D) > cap_floats) break;
     const long long units = (long long)items * s;
     const long long rounds = (units + slots - 1) / slots;
     const double cost = (double)rounds * ((double)NT / s + 4.0) + (s > 1 ? 4.0 * s * items / slots : 0.0);
@@ -502,20 +504,21 @@ int attention_splits(int L, int Lk, int H) {
 }
 
 size_t attention_workspace_floats(int L, int Lk, int H, int D) {
-  const int s = attention_splits(L, Lk, H);
+  const int s = attention_splits(L, Lk, H, D, SIZE_MAX);
   if (s == 1) return 0;
   return (size_t)H * ((L + kQT - 1) / kQT) * s * (size_t)piece_floats(D);
 }
 
 // bf16 requirements (checked by the caller): D in {64, 128}; Q has Mpad >=
 // roundup(L, 256) rows per head; the caches have Lcap >= roundup(Lk, 64) rows
-// whose keys past Lk hold finite values; ws has
-// attention_workspace_floats(L, Lk, H, D) floats.
-void launch_attention(int dtype, const void* q, const void* kc, const void* vt, void* o, float* ws, int L, int Mpad,
-                      int Lcap, int Lk, int H, int D, const int* flag, hipStream_t st) {
+// whose keys past Lk hold finite values; ws holds ws_floats floats (the key
+// split is limited to what fits: attention_workspace_floats(L, Lk, H, D)
+// floats allow the unconstrained choice).
+void launch_attention(int dtype, const void* q, const void* kc, const void* vt, void* o, float* ws, size_t ws_floats,
+                      int L, int Mpad, int Lcap, int Lk, int H, int D, const int* flag, hipStream_t st) {
   if (dtype == 1) {
     const int n_qt = (L + kQT - 1) / kQT;
-    const int n_split = attention_splits(L, Lk, H);
+    const int n_split = attention_splits(L, Lk, H, D, ws != nullptr ? ws_floats : 0);
     const int units = H * n_split * n_qt;
     const int grid = (units + kXcds - 1) / kXcds * kXcds;
     const float sl2 = 1.4426950408889634f / sqrtf((float)D);

@@ -34,6 +34,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -42,9 +43,49 @@
 
 using namespace xc;
 
+// Scratch of xc_forward_chunk_noalloc: the gate's partial records and the
+// attention's key-split partials of one pass, in a static array that every
+// GPU the library runs on holds (one copy per device, at its own address)
+// until the process ends.  In host code `scratch` only names the symbol; its
+// device address comes from hipGetSymbolAddress (device_scratch below).
+constexpr size_t kStaticScratchBytes = (size_t)XC_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+namespace {
+
+// Device address of `scratch` on the current device, looked up once per
+// device (null on failure).
+unsigned char* device_scratch(int device) {
+  static std::mutex mu;
+  static unsigned char* addr[64] = {};
+  if (device < 0 || device >= 64) return nullptr;
+  std::lock_guard<std::mutex> lock(mu);
+  if (addr[device] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    addr[device] = reinterpret_cast<unsigned char*>(p);
+  }
+  return addr[device];
+}
+
+}  // namespace
+
 struct ProfRecord {
   int kind;
   hipEvent_t start, stop;
+};
+
+// Per-pass workspace of the kernels: the gate's per-workgroup partial records
+// and the attention's key-split partials (either the handle's own buffers or
+// the static scratch array of xc_forward_chunk_noalloc).
+struct PassWs {
+  double* records;
+  float* attn;
+  size_t attn_floats;
+  bool prof;   // false: record no kernel timings (xc_profile) in this pass
 };
 
 struct xc_handle {
@@ -93,6 +134,9 @@ struct xc_handle {
   float* x1 = nullptr; float* xa = nullptr; float* xb = nullptr;
   double* fp_records = nullptr;
   float* attn_ws = nullptr;
+  size_t attn_ws_floats = 0;
+  // device address of this GPU's static scratch array (xc_forward_chunk_noalloc)
+  unsigned char* scratch = nullptr;
   // fingerprint tables
   FpTables tables{};
   int n_srows = 0, n_cams = 0, fp_rows = 0, n_wg = 0;
@@ -112,6 +156,7 @@ struct xc_handle {
   bool sticky = false;
   // profiling
   bool profiling = false;
+  bool prof_suspended = false;  // set while a pass must not create events
   std::vector<ProfRecord> prof;
   std::vector<hipEvent_t> ev_free;
   std::vector<void*> allocs;
@@ -325,7 +370,7 @@ void upload(xc_handle* h, const float* src, size_t count, void* dst, bool to_bf1
 // Kernel timing never fails a call: on any event error profiling switches off.
 void prof_begin(xc_handle* h, int kind, ProfRecord* r) {
   r->start = r->stop = nullptr;
-  if (!h->profiling) return;
+  if (!h->profiling || h->prof_suspended) return;
   hipEvent_t e[2];
   for (int i = 0; i < 2; ++i) {
     if (h->ev_free.empty()) {
@@ -385,6 +430,15 @@ GateState gate_state(xc_handle* h) {
   return gs;
 }
 
+PassWs own_ws(xc_handle* h) {
+  PassWs ws;
+  ws.records = h->fp_records;
+  ws.attn = h->attn_ws;
+  ws.attn_floats = h->attn_ws_floats;
+  ws.prof = true;
+  return ws;
+}
+
 template <typename P>
 P* wptr(void* base, size_t elems_before, size_t esz) {
   return reinterpret_cast<P*>(reinterpret_cast<char*>(base) + elems_before * esz);
@@ -393,7 +447,7 @@ P* wptr(void* base, size_t elems_before, size_t esz) {
 // Cross-attention layer of block b on x1 (in place): affine LayerNorm, q
 // projection with the per-head RMSNorm, attention over the condition's keys
 // and values, output projection added without a gate.
-void cross_attention(xc_handle* h, int b, const int* flag) {
+void cross_attention(xc_handle* h, int b, const int* flag, const PassWs& ws) {
   const int C = h->C, H = h->H, D = h->D;
   const int L = (int)h->L;
   const size_t esz = h->esz;
@@ -425,7 +479,8 @@ void cross_attention(xc_handle* h, int b, const int* flag) {
   {
     Prof p(h, XC_KERN_CROSS_ATTENTION);
     launch_attention(h->dtype, h->q, wptr<void>(h->kc_c, (size_t)b * H * h->Lcap_c * D, esz),
-                     wptr<void>(h->vt_c, (size_t)b * H * h->Lcap_c * D, esz), h->o, h->attn_ws, L, (int)h->Mpad,
+                     wptr<void>(h->vt_c, (size_t)b * H * h->Lcap_c * D, esz), h->o, ws.attn, ws.attn_floats, L,
+                     (int)h->Mpad,
                      (int)h->Lcap_c, h->n_cond, H, D, flag, h->st);
   }
   {
@@ -450,7 +505,7 @@ void cross_attention(xc_handle* h, int b, const int* flag) {
 // kv_only: stop after the key/value cache write (the block's output is not
 // needed: the last block of a KV-update pass whose caller takes no output).
 void compute_block(xc_handle* h, int b, const float* x, float* out, const int* flag, void* rhat_tb,
-                   long long kv_off, long long Lk, bool kv_only = false, bool col_sums = false) {
+                   long long kv_off, long long Lk, const PassWs& ws, bool kv_only = false, bool col_sums = false) {
   const int C = h->C, H = h->H, D = h->D, Dm = h->Dm;
   const int L = (int)h->L;
   const size_t esz = h->esz;
@@ -504,8 +559,8 @@ void compute_block(xc_handle* h, int b, const float* x, float* out, const int* f
   if (kv_only) return;
   {
     Prof p(h, XC_KERN_ATTENTION);
-    launch_attention(h->dtype, h->q, kc_b, vt_b, h->o, h->attn_ws, L, (int)h->Mpad, (int)h->Lcap, (int)Lk, H, D, flag,
-                     h->st);
+    launch_attention(h->dtype, h->q, kc_b, vt_b, h->o, ws.attn, ws.attn_floats, L, (int)h->Mpad, (int)h->Lcap, (int)Lk,
+                     H, D, flag, h->st);
   }
   {
     Prof p(h, XC_KERN_GEMM_OPROJ);
@@ -518,7 +573,7 @@ void compute_block(xc_handle* h, int b, const float* x, float* out, const int* f
     e.gate = gate1;
     launch_gemm(h->dtype, EPI_OPROJ, h->o, wptr<void>(h->wo, (size_t)b * C * C, esz), L, C, C, e, flag, h->st);
   }
-  if (h->Mc > 0) cross_attention(h, b, flag);
+  if (h->Mc > 0) cross_attention(h, b, flag, ws);
   {
     Prof p(h, XC_KERN_LN_MOD);
     launch_ln_mod(h->dtype, h->x1, shift2, scale2, h->hbuf, L, C, flag, h->st);
@@ -842,6 +897,7 @@ void init_device(xc_handle* h, const float* w) {
     for (int w = 1; w <= h->Wkv; ++w) ws = std::max(ws, attention_workspace_floats((int)h->L, (int)(w * h->L), H, D));
     for (int n = 1; n <= h->Mc; ++n) ws = std::max(ws, attention_workspace_floats((int)h->L, n, H, D));
     if (ws) h->attn_ws = dalloc_t<float>(h, ws);
+    h->attn_ws_floats = ws;
   }
   if (h->Mc > 0) {
     h->kc_c = dalloc(h, (size_t)B * H * h->Lcap_c * D * esz);
@@ -890,6 +946,85 @@ GateArgs gate_args(xc_handle* h, int t, const float* action) {
   }
   for (int gi = 0; gi < kMaxGroups; ++gi) ga.spatial_count[gi] = h->spatial_count[gi];
   return ga;
+}
+
+xc_status forward_pass(xc_handle* h, int32_t step, float timestep, const float* action_host, const void* x_in,
+                       void* x_out, uint32_t flags, const PassWs& ws) {
+  if (!h || !action_host || !x_in || !x_out) return XC_ERR_INVALID_ARG;
+  if (h->sticky) return XC_ERR_HIP;
+  if (h->Mc > 0 && h->n_cond == 0) return XC_ERR_STATE;
+  if (step < 0 || step >= h->S) return XC_ERR_INVALID_ARG;
+  if ((flags & ~(uint32_t)XC_FORCE_FULL) != 0) return XC_ERR_INVALID_ARG;
+  if (!std::isfinite(timestep)) return XC_ERR_INVALID_ARG;
+  for (int i = 0; i < h->A; ++i)
+    if (!std::isfinite(action_host[i])) return XC_ERR_INVALID_ARG;
+  if (action_changed(h, action_host)) return XC_ERR_STATE;
+  h->prof_suspended = !ws.prof;
+  try {
+    XC_HIP(hipSetDevice(h->device));
+    fix_action(h, action_host);
+    const xc_gate_config& g = h->g;
+    const bool forced_all = !g.enabled || h->n < g.warmup || (flags & XC_FORCE_FULL) ||
+                            (step == 0 && g.step0_mode == XC_STEP0_FORCE);
+    pass_conditioning(h, timestep, action_host);
+    GateState gs = gate_state(h);
+    launch_pass_begin(gs, h->B, h->st);
+    const long long kv_off = (h->n % h->Wkv) * h->L;
+    const long long Lk = std::min<long long>(h->n + 1, h->Wkv) * h->L;
+    const GateArgs ga = gate_args(h, step, action_host);
+    const float* x = reinterpret_cast<const float*>(x_in);
+    for (int b = 0; b < h->B; ++b) {
+      float* out = b == h->B - 1 ? reinterpret_cast<float*>(x_out) : ((b & 1) ? h->xb : h->xa);
+      const int* flag = nullptr;
+      void* rhat_tb = nullptr;
+      if (gateable(h, b)) {
+        const size_t sb = (size_t)step * h->B + b;
+        rhat_tb = wptr<void>(h->rhat, sb * h->L * h->C, h->esz);
+        const bool evaluate = !forced_all && h->visited[sb];
+        {
+          Prof p(h, XC_KERN_GATE);
+          const size_t fo = sb * h->fp_rows * h->C;
+          FoldArgs fa{};
+          fa.full = (h->fold && b >= 1) ? 0 : 1;
+          fa.b = b;
+          fa.prev_gateable = b >= 1 && gateable(h, b - 1);
+          fa.flags = h->flags;
+          if (h->fold) {
+            fa.csum_part = h->csum_part;
+            fa.n_rb = h->n_rb;
+            fa.cam_rb_lo = h->cam_rb_lo;
+            fa.cam_rb_hi = h->cam_rb_hi;
+            fa.rb_cam = h->rb_cam;
+            fa.csum_in = h->csum_in;
+            fa.csum_rhat = h->csum_rhat + (size_t)step * h->B * h->n_cams * h->C;
+          }
+          launch_fp_compare(x, h->C, h->tables, h->fp + fo, h->fp_alt ? h->fp_alt + fo : nullptr,
+                            h->fp_sel ? h->fp_sel + sb : nullptr, ws.records, fa, h->st);
+        }
+        {
+          Prof p(h, XC_KERN_GATE_DECIDE);
+          launch_gate_decide(ws.records, h->n_wg, ga, gs, (int)sb, b, evaluate ? 1 : 0, h->st);
+        }
+        h->visited[sb] = 1;
+        if (evaluate) {
+          ++h->gated_evals;
+          flag = h->flags + b;  // the block's first LayerNorm kernel also runs the skip path
+        }
+      }
+      compute_block(h, b, x, out, flag, rhat_tb, kv_off, Lk, ws, false, b + 1 < h->B && gateable(h, b + 1));
+      x = out;
+    }
+    if (h->n >= g.warmup) h->evals_post_warmup += h->B;
+    h->last_step = step;
+    h->any_forward = true;
+    if (check_launch() != XC_OK) throw Fail{XC_ERR_HIP};
+  } catch (const Fail& f) {
+    h->prof_suspended = false;
+    if (f.s == XC_ERR_HIP) h->sticky = true;
+    return f.s;
+  }
+  h->prof_suspended = false;
+  return XC_OK;
 }
 
 }  // namespace
@@ -947,6 +1082,8 @@ xc_status xc_init(const xc_model_config* model, const xc_gate_config* gate, cons
   h->Lcap_c = ((long long)h->Mc + 63) / 64 * 64;
   try {
     XC_HIP(hipGetDevice(&h->device));
+    // null if the lookup failed: xc_forward_chunk_noalloc then returns XC_ERR_STATE
+    h->scratch = device_scratch(h->device);
     init_device(h, weights_host);
   } catch (const Fail& f) {
     (void)hipGetLastError();
@@ -964,78 +1101,23 @@ xc_status xc_init(const xc_model_config* model, const xc_gate_config* gate, cons
 
 xc_status xc_forward_chunk(xc_handle* h, int32_t step, float timestep, const float* action_host, const void* x_in,
                            void* x_out, uint32_t flags) {
-  if (!h || !action_host || !x_in || !x_out) return XC_ERR_INVALID_ARG;
-  if (h->sticky) return XC_ERR_HIP;
-  if (h->Mc > 0 && h->n_cond == 0) return XC_ERR_STATE;
-  if (step < 0 || step >= h->S) return XC_ERR_INVALID_ARG;
-  if ((flags & ~(uint32_t)XC_FORCE_FULL) != 0) return XC_ERR_INVALID_ARG;
-  if (!std::isfinite(timestep)) return XC_ERR_INVALID_ARG;
-  for (int i = 0; i < h->A; ++i)
-    if (!std::isfinite(action_host[i])) return XC_ERR_INVALID_ARG;
-  if (action_changed(h, action_host)) return XC_ERR_STATE;
-  try {
-    XC_HIP(hipSetDevice(h->device));
-    fix_action(h, action_host);
-    const xc_gate_config& g = h->g;
-    const bool forced_all = !g.enabled || h->n < g.warmup || (flags & XC_FORCE_FULL) ||
-                            (step == 0 && g.step0_mode == XC_STEP0_FORCE);
-    pass_conditioning(h, timestep, action_host);
-    GateState gs = gate_state(h);
-    launch_pass_begin(gs, h->B, h->st);
-    const long long kv_off = (h->n % h->Wkv) * h->L;
-    const long long Lk = std::min<long long>(h->n + 1, h->Wkv) * h->L;
-    const GateArgs ga = gate_args(h, step, action_host);
-    const float* x = reinterpret_cast<const float*>(x_in);
-    for (int b = 0; b < h->B; ++b) {
-      float* out = b == h->B - 1 ? reinterpret_cast<float*>(x_out) : ((b & 1) ? h->xb : h->xa);
-      const int* flag = nullptr;
-      void* rhat_tb = nullptr;
-      if (gateable(h, b)) {
-        const size_t sb = (size_t)step * h->B + b;
-        rhat_tb = wptr<void>(h->rhat, sb * h->L * h->C, h->esz);
-        const bool evaluate = !forced_all && h->visited[sb];
-        {
-          Prof p(h, XC_KERN_GATE);
-          const size_t fo = sb * h->fp_rows * h->C;
-          FoldArgs fa{};
-          fa.full = (h->fold && b >= 1) ? 0 : 1;
-          fa.b = b;
-          fa.prev_gateable = b >= 1 && gateable(h, b - 1);
-          fa.flags = h->flags;
-          if (h->fold) {
-            fa.csum_part = h->csum_part;
-            fa.n_rb = h->n_rb;
-            fa.cam_rb_lo = h->cam_rb_lo;
-            fa.cam_rb_hi = h->cam_rb_hi;
-            fa.rb_cam = h->rb_cam;
-            fa.csum_in = h->csum_in;
-            fa.csum_rhat = h->csum_rhat + (size_t)step * h->B * h->n_cams * h->C;
-          }
-          launch_fp_compare(x, h->C, h->tables, h->fp + fo, h->fp_alt ? h->fp_alt + fo : nullptr,
-                            h->fp_sel ? h->fp_sel + sb : nullptr, h->fp_records, fa, h->st);
-        }
-        {
-          Prof p(h, XC_KERN_GATE_DECIDE);
-          launch_gate_decide(h->fp_records, h->n_wg, ga, gs, (int)sb, b, evaluate ? 1 : 0, h->st);
-        }
-        h->visited[sb] = 1;
-        if (evaluate) {
-          ++h->gated_evals;
-          flag = h->flags + b;  // the block's first LayerNorm kernel also runs the skip path
-        }
-      }
-      compute_block(h, b, x, out, flag, rhat_tb, kv_off, Lk, false, b + 1 < h->B && gateable(h, b + 1));
-      x = out;
-    }
-    if (h->n >= g.warmup) h->evals_post_warmup += h->B;
-    h->last_step = step;
-    h->any_forward = true;
-    if (check_launch() != XC_OK) throw Fail{XC_ERR_HIP};
-  } catch (const Fail& f) {
-    if (f.s == XC_ERR_HIP) h->sticky = true;
-    return f.s;
-  }
-  return XC_OK;
+  if (!h) return XC_ERR_INVALID_ARG;
+  return forward_pass(h, step, timestep, action_host, x_in, x_out, flags, own_ws(h));
+}
+
+xc_status xc_forward_chunk_noalloc(xc_handle* h, int32_t step, float timestep, const float* action_host,
+                                   const void* x_in, void* x_out, uint32_t flags) {
+  if (!h) return XC_ERR_INVALID_ARG;
+  if (h->scratch == nullptr) return XC_ERR_STATE;
+  // the gate's records first, the attention partials in the rest (256-byte aligned)
+  const size_t rec_bytes = ((size_t)h->n_wg * kMaxGroups * kFpRecord * sizeof(double) + 255) / 256 * 256;
+  if (rec_bytes > kStaticScratchBytes) return XC_ERR_UNSUPPORTED;
+  PassWs ws;
+  ws.records = reinterpret_cast<double*>(h->scratch);
+  ws.attn = reinterpret_cast<float*>(h->scratch + rec_bytes);
+  ws.attn_floats = (kStaticScratchBytes - rec_bytes) / sizeof(float);
+  ws.prof = false;
+  return forward_pass(h, step, timestep, action_host, x_in, x_out, flags, ws);
 }
 
 xc_status xc_kv_update(xc_handle* h, float timestep, const float* action_host, const void* x_clean, void* x_out) {
@@ -1055,7 +1137,7 @@ xc_status xc_kv_update(xc_handle* h, float timestep, const float* action_host, c
     for (int b = 0; b < h->B; ++b) {
       float* out = (b & 1) ? h->xb : h->xa;
       if (b == h->B - 1 && x_out) out = reinterpret_cast<float*>(x_out);
-      compute_block(h, b, x, out, nullptr, nullptr, kv_off, Lk, b == h->B - 1 && !x_out);
+      compute_block(h, b, x, out, nullptr, nullptr, kv_off, Lk, own_ws(h), b == h->B - 1 && !x_out);
       x = out;
     }
     h->kv_block_evals += h->B;

@@ -168,8 +168,11 @@ void launch_rope_table(float2* tab, const RopeArgs& r, int n_slots, const int* s
 // Floats of the attention workspace (partials of items whose keys are split
 // across workgroups) for L queries over Lk keys, H heads of dimension D.
 size_t attention_workspace_floats(int L, int Lk, int H, int D);
-void launch_attention(int dtype, const void* q, const void* kring, const void* vtring, void* o, float* ws, int L,
-                      int Mpad, int Lcap, int Lk, int H, int D, const int* flag, hipStream_t st);
+// ws: ws_floats floats of workspace; the key split is chosen among those
+// whose partials fit (none: no split).
+void launch_attention(int dtype, const void* q, const void* kring, const void* vtring, void* o, float* ws,
+                      size_t ws_floats, int L, int Mpad, int Lcap, int Lk, int H, int D, const int* flag,
+                      hipStream_t st);
 void launch_axpby(float a, const float* x, float b, const float* y, float* out, long long n, hipStream_t st);
 void launch_pass_begin(const GateState& gs, int n_blocks, hipStream_t st);
 // Gated evaluation, first launch: fingerprint of x against the (t, b) cache

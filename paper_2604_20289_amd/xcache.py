@@ -33,7 +33,8 @@ XC_MAX_GROUPS = 8
 KERNEL_NAMES = ["attention", "gemm_qkv", "gemm_oproj", "gemm_up", "gemm_down", "gate", "gate_decide", "skip_add",
                 "ln_mod", "qk_norm", "adaln", "cross_q", "cross_attention", "cross_o"]
 
-EXPORTED = ["xc_status_string", "xc_init", "xc_forward_chunk", "xc_kv_update", "xc_set_condition", "xc_stats",
+EXPORTED = ["xc_status_string", "xc_init", "xc_forward_chunk", "xc_forward_chunk_noalloc", "xc_kv_update",
+            "xc_set_condition", "xc_stats",
             "xc_reset", "xc_destroy", "xc_axpby", "xc_fingerprint_rows", "xc_profile", "xc_kernel_times"]
 
 
@@ -92,6 +93,7 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
         "xc_status_string": (ctypes.c_char_p, [i32]),
         "xc_init": (i32, [P(ModelConfigC), P(GateConfigC), vp, sz, vp, P(vp)]),
         "xc_forward_chunk": (i32, [vp, i32, f32, vp, vp, vp, u32]),
+        "xc_forward_chunk_noalloc": (i32, [vp, i32, f32, vp, vp, vp, u32]),
         "xc_kv_update": (i32, [vp, f32, vp, vp, vp]),
         "xc_set_condition": (i32, [vp, vp, i32]),
         "xc_stats": (i32, [vp, P(StatsC), vp, vp, vp, vp, vp, vp]),
@@ -177,6 +179,12 @@ def xc_forward_chunk(h: int, step: int, timestep: float, action: np.ndarray, x_i
            "xc_forward_chunk")
 
 
+def xc_forward_chunk_noalloc(h: int, step: int, timestep: float, action: np.ndarray, x_in, x_out, flags: int = 0):
+    a = np.ascontiguousarray(action, dtype=np.float32)
+    _check(load_library().xc_forward_chunk_noalloc(h, step, timestep, a.ctypes.data, _ptr(x_in), _ptr(x_out), flags),
+           "xc_forward_chunk_noalloc")
+
+
 def xc_kv_update(h: int, timestep: float, action: np.ndarray, x_clean, x_out=None):
     a = np.ascontiguousarray(action, dtype=np.float32)
     _check(load_library().xc_kv_update(h, timestep, a.ctypes.data, _ptr(x_clean), _ptr(x_out)), "xc_kv_update")
@@ -256,6 +264,9 @@ class XCache:
 
     def forward_chunk(self, step: int, timestep: float, action, x_in, x_out, flags: int = 0):
         xc_forward_chunk(self.h, step, timestep, action, x_in, x_out, flags)
+
+    def forward_chunk_noalloc(self, step: int, timestep: float, action, x_in, x_out, flags: int = 0):
+        xc_forward_chunk_noalloc(self.h, step, timestep, action, x_in, x_out, flags)
 
     def set_condition(self, cond):
         xc_set_condition(self.h, cond)
