@@ -263,6 +263,31 @@ xc_status xc_kv_update(xc_handle* h, float timestep, const float* action_host,
  * Synchronises the stream once (the upload). */
 xc_status xc_set_condition(xc_handle* h, const float* cond_host, int32_t n_tokens);
 
+/* Caches readable with xc_read_cache. */
+enum { XC_CACHE_RESIDUAL = 0, XC_CACHE_KEYS = 1, XC_CACHE_VALUES = 2 };
+
+/* Copies one of the handle's caches, as float32, into a caller device buffer
+ * (enqueued on the bound stream; does not synchronise).  For bf16 models the
+ * values are the stored bf16 numbers.
+ *   XC_CACHE_RESIDUAL : the cached residual r_hat of (t = step, b = block),
+ *                       Eq. 3, [L][C]; unspecified until (t, b) has computed
+ *                       once.
+ *   XC_CACHE_KEYS     : block b's rolling key cache (Section 2.1) as
+ *                       [H][kv_window * L][d]: keys after the QK RMSNorm (and
+ *                       the rotation with rope = 1); rows [s L, (s + 1) L)
+ *                       hold the latest generation n with n mod kv_window ==
+ *                       s -- the current generation's slot holds its latest
+ *                       pass's keys until xc_kv_update writes the clean ones.
+ *                       step is ignored.
+ *   XC_CACHE_VALUES   : block b's value cache, same layout.
+ *   out_dev    : device float32 buffer of out_floats elements, which must be
+ *                the tensor's element count.
+ * Errors: XC_ERR_INVALID_ARG (NULL, kind / step / block out of range, size
+ * mismatch), XC_ERR_STATE (the residual of a block the gate never evaluates),
+ * XC_ERR_HIP (sticky). */
+xc_status xc_read_cache(xc_handle* h, int32_t kind, int32_t step, int32_t block, void* out_dev,
+                        size_t out_floats);
+
 /* Synchronise the stream and copy out counters and per-(t, b) state.
  * Every array pointer may be NULL.  skip_counts: int32 [S * B] (t-major);
  * last_decision: uint8 [B] for the last denoising pass (XC_DEC_*;

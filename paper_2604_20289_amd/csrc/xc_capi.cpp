@@ -1245,6 +1245,39 @@ xc_status xc_stats(xc_handle* h, xc_stats_t* stats, int32_t* skip_counts, uint8_
   return XC_OK;
 }
 
+xc_status xc_read_cache(xc_handle* h, int32_t kind, int32_t step, int32_t block, void* out_dev, size_t out_floats) {
+  if (!h || !out_dev) return XC_ERR_INVALID_ARG;
+  if (h->sticky) return XC_ERR_HIP;
+  if (block < 0 || block >= h->B) return XC_ERR_INVALID_ARG;
+  if (kind == XC_CACHE_RESIDUAL) {
+    if (step < 0 || step >= h->S) return XC_ERR_INVALID_ARG;
+    if (!gateable(h, block) || h->rhat == nullptr) return XC_ERR_STATE;
+    if (out_floats != (size_t)h->L * h->C) return XC_ERR_INVALID_ARG;
+  } else if (kind == XC_CACHE_KEYS || kind == XC_CACHE_VALUES) {
+    if (out_floats != (size_t)h->H * h->Wkv * h->L * h->D) return XC_ERR_INVALID_ARG;
+  } else {
+    return XC_ERR_INVALID_ARG;
+  }
+  try {
+    XC_HIP(hipSetDevice(h->device));
+    float* out = reinterpret_cast<float*>(out_dev);
+    if (kind == XC_CACHE_RESIDUAL) {
+      const size_t sb = (size_t)step * h->B + block;
+      launch_read_cache(h->dtype, wptr<void>(h->rhat, sb * h->L * h->C, h->esz), out, 1, (int)h->L, h->C, h->L, 0,
+                        h->st);
+    } else {
+      const void* src = wptr<void>(kind == XC_CACHE_KEYS ? h->kc : h->vt, (size_t)block * h->H * h->Lcap * h->D, h->esz);
+      launch_read_cache(h->dtype, src, out, h->H, (int)(h->Wkv * h->L), h->D, h->Lcap, kind == XC_CACHE_VALUES ? 1 : 0,
+                        h->st);
+    }
+    if (check_launch() != XC_OK) throw Fail{XC_ERR_HIP};
+  } catch (const Fail& f) {
+    h->sticky = true;
+    return f.s;
+  }
+  return XC_OK;
+}
+
 xc_status xc_reset(xc_handle* h) {
   if (!h) return XC_ERR_INVALID_ARG;
   if (h->sticky) return XC_ERR_HIP;

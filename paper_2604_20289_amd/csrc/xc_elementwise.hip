@@ -298,6 +298,19 @@ __global__ void axpby_kernel(float a, const float* __restrict__ x, float b, cons
     out[i] = a * x[i] + b * y[i];
 }
 
+// out[h][r][d] (float32, r < R) from a cache stored [H][Lcap][D] or, when
+// transposed, [H][D][Lcap] (row r is column r)
+template <typename T>
+__global__ void read_cache_kernel(const T* __restrict__ src, float* __restrict__ out, int R, int D, long long Lcap,
+                                  int transposed, long long n) {
+  for (long long i = blockIdx.x * 256ll + threadIdx.x; i < n; i += (long long)gridDim.x * 256) {
+    const long long hr = i / D, h = hr / R;
+    const int d = (int)(i - hr * D), r = (int)(hr - h * R);
+    const long long j = transposed ? ((h * D + d) * Lcap + r) : ((h * Lcap + r) * D + d);
+    out[i] = (float)src[j];
+  }
+}
+
 __global__ void fill_f32_kernel(float* p, float v, long long n) {
   for (long long i = blockIdx.x * 256ll + threadIdx.x; i < n; i += (long long)gridDim.x * 256) p[i] = v;
 }
@@ -381,6 +394,15 @@ void launch_rope_table(float2* tab, const RopeArgs& r, int n_slots, const int* s
 
 void launch_axpby(float a, const float* x, float b, const float* y, float* out, long long n, hipStream_t st) {
   axpby_kernel<<<grid_for(n, 256 * 4), 256, 0, st>>>(a, x, b, y, out, n);
+}
+
+void launch_read_cache(int dtype, const void* src, float* out, int H, int R, int D, long long Lcap, int transposed,
+                       hipStream_t st) {
+  const long long n = (long long)H * R * D;
+  if (dtype == 1)
+    read_cache_kernel<bf16><<<grid_for(n, 256 * 4), 256, 0, st>>>((const bf16*)src, out, R, D, Lcap, transposed, n);
+  else
+    read_cache_kernel<float><<<grid_for(n, 256 * 4), 256, 0, st>>>((const float*)src, out, R, D, Lcap, transposed, n);
 }
 
 void launch_fill_f32(float* p, float v, long long n, hipStream_t st) {

@@ -187,5 +187,9 @@ void launch_fp_compare(const float* x, int C, const FpTables& t, float* fp0, flo
 void launch_gate_decide(const double* records, int n_wg, const GateArgs& ga, const GateState& gs, int sb, int b,
                         int evaluate, hipStream_t st);
 void launch_fill_f32(float* p, float v, long long n, hipStream_t st);
+// out [H][R][D] float32 from a model-dtype cache [H][Lcap][D] (transposed = 0)
+// or [H][D][Lcap] (transposed = 1), rows 0 .. R-1
+void launch_read_cache(int dtype, const void* src, float* out, int H, int R, int D, long long Lcap, int transposed,
+                       hipStream_t st);
 
 }  // namespace xc

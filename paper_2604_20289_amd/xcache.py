@@ -25,6 +25,7 @@ XC_FP_GRID3D, XC_FP_LINSPACE1D = 0, 1
 XC_FP_REFRESH_EVERY, XC_FP_REFRESH_ON_COMPUTE = 0, 1
 XC_FORCE_FULL = 1
 XC_DEC_COMPUTE, XC_DEC_SKIP, XC_DEC_FORCED, XC_DEC_NONE = 0, 1, 2, 255
+XC_CACHE_RESIDUAL, XC_CACHE_KEYS, XC_CACHE_VALUES = 0, 1, 2
 XC_MAX_GROUPS = 8
 (XC_KERN_ATTENTION, XC_KERN_GEMM_QKV, XC_KERN_GEMM_OPROJ, XC_KERN_GEMM_UP, XC_KERN_GEMM_DOWN,
  XC_KERN_GATE, XC_KERN_GATE_DECIDE, XC_KERN_SKIP_ADD, XC_KERN_LN_MOD, XC_KERN_QK_NORM, XC_KERN_ADALN,
@@ -34,7 +35,7 @@ KERNEL_NAMES = ["attention", "gemm_qkv", "gemm_oproj", "gemm_up", "gemm_down", "
                 "ln_mod", "qk_norm", "adaln", "cross_q", "cross_attention", "cross_o"]
 
 EXPORTED = ["xc_status_string", "xc_init", "xc_forward_chunk", "xc_forward_chunk_noalloc", "xc_kv_update",
-            "xc_set_condition", "xc_stats",
+            "xc_set_condition", "xc_read_cache", "xc_stats",
             "xc_reset", "xc_destroy", "xc_axpby", "xc_fingerprint_rows", "xc_profile", "xc_kernel_times"]
 
 
@@ -96,6 +97,7 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
         "xc_forward_chunk_noalloc": (i32, [vp, i32, f32, vp, vp, vp, u32]),
         "xc_kv_update": (i32, [vp, f32, vp, vp, vp]),
         "xc_set_condition": (i32, [vp, vp, i32]),
+        "xc_read_cache": (i32, [vp, i32, i32, i32, vp, sz]),
         "xc_stats": (i32, [vp, P(StatsC), vp, vp, vp, vp, vp, vp]),
         "xc_reset": (i32, [vp]),
         "xc_destroy": (i32, [vp]),
@@ -197,6 +199,10 @@ def xc_set_condition(h: int, cond: np.ndarray):
     _check(load_library().xc_set_condition(h, c.ctypes.data, c.shape[0]), "xc_set_condition")
 
 
+def xc_read_cache(h: int, kind: int, step: int, block: int, out, n_floats: int):
+    _check(load_library().xc_read_cache(h, kind, step, block, _ptr(out), n_floats), "xc_read_cache")
+
+
 def xc_stats(h: int, n_steps: int, n_blocks: int) -> dict:
     st = StatsC()
     counts = np.zeros(n_steps * n_blocks, np.int32)
@@ -276,6 +282,10 @@ class XCache:
 
     def stats(self) -> dict:
         return xc_stats(self.h, self.S, self.B)
+
+    def read_cache(self, kind: int, step: int, block: int, out):
+        """Copy a cache into the float32 device tensor ``out`` (see xc_read_cache)."""
+        xc_read_cache(self.h, kind, step, block, out, out.numel())
 
     def reset(self):
         xc_reset(self.h)

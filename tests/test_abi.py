@@ -143,6 +143,8 @@ def test_calls_on_null_handle():
     assert lib.xc_axpby(None, 1.0, 1, 1.0, 1, 1, 4) == xcp.XC_ERR_INVALID_ARG
     assert lib.xc_profile(None, 1) == xcp.XC_ERR_INVALID_ARG
     assert lib.xc_set_condition(None, a.ctypes.data, 1) == xcp.XC_ERR_INVALID_ARG
+    assert lib.xc_forward_chunk_noalloc(None, 0, 1.0, a.ctypes.data, 1, 1, 0) == xcp.XC_ERR_INVALID_ARG
+    assert lib.xc_read_cache(None, xcp.XC_CACHE_KEYS, 0, 0, 1, 1) == xcp.XC_ERR_INVALID_ARG
 
 
 def test_weight_blob_size_includes_cross_attention_tensors():

@@ -187,3 +187,139 @@ def test_multicamera_extended_block_fullsize():
         assert err <= 2e-2
     finally:
         xc.close()
+
+
+def _progress(line):
+    """Progress of a long test, printed and appended to gpurun_out/ (pytest -q
+    shows nothing until a test ends)."""
+    import os
+    print(line, flush=True)
+    d = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "gpurun_out")
+    os.makedirs(d, exist_ok=True)
+    with open(os.path.join(d, "progress_fullsize.log"), "a") as f:
+        f.write(line + "\n")
+
+
+def test_multicamera_steady_state_window_and_skips():
+    """The multi-camera shapes (L = 7020, hidden 1536, 12 heads x 128, MLP 6144),
+    two gated blocks (no front anchor), fixed cosine threshold 0.9 on a
+    rho = 0.999 stream, four chunks:
+
+    * chunk 0 (warmup): every block computes; outputs, pass residuals and both
+      blocks' cached residuals r_hat against the oracle;
+    * chunks 1-3: both blocks skip outside the band (s about 0.999 against 0.9),
+      so each pass is x + r_hat of both blocks (Eq. 4) -- the skip path at
+      full width, and block 1's gate taking its global channel from block 0's
+      skip identity;
+    * every KV-update pass: its output and both blocks' key/value caches; the
+      window grows to 21060 keys (chunk 2) and chunk 3 reuses ring slot 0 (FIFO);
+    * chunk 3 step 3 is forced (XC_FORCE_FULL): both blocks compute over the
+      full 21060-key window with slot 0 holding the current chunk.
+
+    The oracle computes in float32 (bf16 storage rounding); the last block of
+    the two passes at 21060 keys is compared on sampled token rows (the
+    oracle's row-restricted mode).  Relative L2 2e-2 throughout."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from lockstep import in_band, rel_l2
+    from paper_2604_20289_amd.xcache import (XC_CACHE_KEYS, XC_CACHE_RESIDUAL, XC_CACHE_VALUES, XC_FORCE_FULL,
+                                             XCache)
+
+    w = synth.with_stream(synth.with_model(synth.with_gate(synth.workload(2), front_anchors=0, adaptive=0,
+                                                           tau_cos_fixed=0.9), n_blocks=2), rho=0.999)
+    m = w.model
+    L, C, H, d, W, S = m.tokens, m.hidden, m.n_heads, m.head_dim, m.kv_window, m.n_steps
+    rows = np.unique(np.concatenate([np.linspace(0, L - 1, 61).astype(int), np.arange(0, L, 1170),
+                                     np.arange(1169, L, 1170)]))
+    blob = synth.make_weights(m)
+    _progress(f"[steady] L={L} C={C} blocks={m.n_blocks} window={W * L} keys, rows sampled={len(rows)}")
+    xc = XCache(m, w.gate, blob, torch.cuda.current_stream().cuda_stream)
+    orc = xo.XCacheOracle(m, w.gate, blob, compute=np.float32)
+    n_chunks = 4
+    eps = list(synth.latent_stream(m, w.stream, 0, n_chunks))
+    acts = list(synth.action_stream(m, w.stream, 0, n_chunks))
+    taus = synth.timesteps(m)
+    dev = torch.device("cuda")
+    x_d = torch.empty((L, C), dtype=torch.float32, device=dev)
+    y_d = torch.empty_like(x_d)
+    k_d = torch.empty_like(x_d)
+    r_d = torch.empty_like(x_d)
+    kv_d = torch.empty((H * W * L * d,), dtype=torch.float32, device=dev)
+    tol = 2e-2
+    worst = {}
+
+    def check(tag, got, want):
+        e = rel_l2(got, want)
+        worst[tag.split()[0]] = max(worst.get(tag.split()[0], 0.0), e)
+        assert e <= tol, f"{tag}: rel-L2 {e:.3e}"
+        return e
+
+    def check_ring(n):
+        for b in range(m.n_blocks):
+            for kind, idx in ((XC_CACHE_KEYS, 0), (XC_CACHE_VALUES, 1)):
+                xc.read_cache(kind, 0, b, kv_d)
+                got = kv_d.cpu().numpy().reshape(H, W * L, d)
+                ring = orc.ring[b]
+                for i, entry in enumerate(ring):
+                    g = n - (len(ring) - 1) + i
+                    check(f"kv-cache n={n} b={b} gen={g} {'KV'[idx]}", got[:, (g % W) * L:(g % W + 1) * L], entry[idx])
+
+    def decide_from(st):
+        def decide(b, info):
+            dev_skip = int(st["last_decision"][b]) == xo.DEC_SKIP
+            if dev_skip != bool(info["skip"]):
+                assert in_band(info, w.gate.tau_dev), (b, info, st["last_cos"][b], st["last_dev"][b])
+            return dev_skip
+        return decide
+
+    try:
+        for n in range(n_chunks):
+            x_d.copy_(torch.from_numpy(eps[n]).to(dev))
+            eps_d = x_d.clone()
+            x_o = eps[n].astype(np.float32)
+            for t in range(S):
+                last = n == n_chunks - 1 and t == S - 1
+                f = XC_FORCE_FULL if last else 0
+                xc.forward_chunk(t, taus[t], acts[n], x_d, y_d, f)
+                st = xc.stats()
+                y_o = orc.forward_chunk(t, taus[t], acts[n], x_o, f, decide=decide_from(st),
+                                        rows=rows if last else None)
+                dec = [int(v) for v in st["last_decision"]]
+                assert dec == [i["decision"] for i in orc.last], (n, t, dec)
+                if n >= 1 and not last:
+                    assert dec == [xo.DEC_SKIP] * m.n_blocks, (n, t, dec)
+                y = y_d.cpu().numpy()
+                xin = x_d.cpu().numpy()
+                sel = rows if last else slice(None)
+                e1 = check(f"y n={n} t={t}", y[sel], y_o)
+                e2 = check(f"y-x n={n} t={t}", (y - xin)[sel], y_o - x_o[sel])
+                for b in range(m.n_blocks):
+                    if dec[b] != xo.DEC_SKIP and not (last and b == m.n_blocks - 1):
+                        xc.read_cache(XC_CACHE_RESIDUAL, t, b, r_d)
+                        check(f"r_hat n={n} t={t} b={b}", r_d.cpu().numpy(), orc.rhat[(t, b)])
+                _progress(f"[steady] n={n} t={t} decisions={dec} s={[round(float(v), 5) for v in st['last_cos']]} "
+                          f"rel-L2 y {e1:.2e} y-x {e2:.2e}")
+                if last:
+                    break
+                if t + 1 < S:
+                    sg = synth.sampler_sigma(m, t + 1)
+                    xc.axpby(1.0 - sg, y_d, sg, eps_d, x_d, L * C)
+                    x_o = ((1.0 - sg) * y_o + sg * eps[n].astype(np.float32)).astype(np.float32)
+            if n == n_chunks - 1:
+                break
+            xc.kv_update(0.0, acts[n], y_d, k_d)
+            restrict = n >= 2                  # 21060 keys: last block on sampled rows
+            k_o = orc.kv_update(0.0, acts[n], y_o, rows=rows if restrict else None)
+            k = k_d.cpu().numpy()
+            sel = rows if restrict else slice(None)
+            e1 = check(f"kv n={n}", k[sel], k_o)
+            e2 = check(f"kv-res n={n}", (k - y_d.cpu().numpy())[sel], k_o - y_o[sel])
+            check_ring(n)
+            _progress(f"[steady] n={n} kv-update ({min(n + 1, W) * L} keys) rel-L2 {e1:.2e} residual {e2:.2e}; "
+                      f"ring slots checked")
+        st = xc.stats()
+        _progress(f"[steady] skips={st['skips']} worst={ {k: f'{v:.2e}' for k, v in worst.items()} }")
+        assert st["skips"] == 2 * S * m.n_blocks + (S - 1) * m.n_blocks  # chunks 1-2 every step, chunk 3 steps 0-2
+        assert st["skips"] == orc.skips
+    finally:
+        xc.close()

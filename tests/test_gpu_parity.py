@@ -169,6 +169,46 @@ def test_bf16_head64_always_skip_and_table1():
             ls.close()
 
 
+# widths whose LayerNorm launch (which also runs the skip path, Eq. 4) takes
+# the 8- and 16-vector-per-lane instantiations: the multi-camera hidden size
+# 1536 (MLP 6144) and 4096 (MLP 1024 to keep the oracle quick); two cameras of
+# 150 tokens, so the gate's global channel comes from the MLP-down column sums
+BF_WIDE = {
+    1536: synth.Workload(
+        "bf16-wide-3blk-h1536-L300",
+        synth.ModelShape(3, 1536, 12, 128, 6144, 256, 16, synth.BF16, 4, 2, (synth.ViewGroup(2, 1, 10, 15),)),
+        synth.GateParams(),
+        synth.StreamParams(4, 0.999, 0.02)),
+    4096: synth.Workload(
+        "bf16-wide-2blk-h4096-L300",
+        synth.ModelShape(2, 4096, 32, 128, 1024, 256, 16, synth.BF16, 4, 2, (synth.ViewGroup(2, 1, 10, 15),)),
+        synth.GateParams(),
+        synth.StreamParams(3, 0.999, 0.02)),
+}
+
+
+@pytest.mark.parametrize("width", sorted(BF_WIDE))
+@pytest.mark.parametrize("gate", ["always-skip", "table1"])
+def test_bf16_wide_skip_path(width, gate):
+    """Skipped blocks at C >= 1024 against the oracle: the pass output, the pass
+    residual, every refreshed r_hat and the key/value caches, with skips > 0."""
+    w = BF_WIDE[width]
+    if gate == "always-skip":
+        w = synth.with_gate(w, adaptive=0, tau_cos_fixed=-1.0, tau_dev=math.inf)
+    ls = _ls(w, compute=np.float32)
+    try:
+        st = ls.run(w.stream.n_chunks, tol_rel_l2=TOLBF)
+        print(f"[parity] {w.name} {gate}: skips={st['skips']} of {st['evals_post_warmup']} band={ls.band_hits} "
+              f"r_hat checked={ls.residuals_checked} kv slots={ls.kv_slots_checked} "
+              f"worst={max(ls.worst.values()):.2e}", flush=True)
+        assert st["skips"] > 0
+        if gate == "always-skip":
+            B, S = w.model.n_blocks, w.model.n_steps
+            assert st["skips"] == (w.stream.n_chunks - 1) * S * (B - 1)
+    finally:
+        ls.close()
+
+
 @pytest.mark.slow
 def test_cfg1_prefix_parity():
     """Single-camera bf16 configuration, first 4 chunks, Table-1 gate."""
