@@ -12,13 +12,20 @@ defaults.
 Runs, in order:
   1. gate on, `warmup` untimed chunks then `steps` timed chunks -> mean
      chunk latency (the reported value; the paper reports the average
-     per-chunk DiT time) and block skip rate;
-  2. gate off (every block computed, same kernels), same chunks ->
+     per-chunk DiT time) and the block skip rate over the timed chunks;
+  2. the skip path alone (a gate that skips every block after the warmup
+     chunk) -> time per skipped block and the per-launch averages of its
+     kernels; the gate comparison that reads the block input, with that
+     input in the last-level cache and after a 1 GiB write evicted it;
+  3. the same stream at tau_floor 0.95 (the value the paper's Section 2.4
+     text gives; Table 1 says 0.97);
+  4. gate off (every block computed, same kernels), same chunks ->
      full-compute latency and effective block TFLOP/s; then the same chunks
      again with HIP events around every kernel launch -> per-kernel
      durations and the roofline of the dominant kernel (attention);
-  3. gate on again for two chunks with kernel events -> gate-kernel GB/s;
-  4. the CPU oracle on a bounded sample (one computed block at the full
+  5. the gate-stress stream (same shapes; scene cut every 8th chunk, a
+     steering step every 5th) -> its latency and skip rate;
+  6. the CPU oracle on a bounded sample (one computed block at the full
      shape, float64 numpy on the host cores), scaled to ms per chunk.
 Prints one JSON line.
 """
@@ -80,12 +87,16 @@ def attention_flops(m, n_keys):
     return 4.0 * m.tokens * n_keys * m.n_heads * m.head_dim
 
 
-def run_stream(xc, m, eps_dev, actions, n_warm, n_timed, torch, profile=False, force_every=0, per_chunk=None):
+def run_stream(xc, m, eps_dev, actions, n_warm, n_timed, torch, profile=False, force_every=0, per_chunk=None,
+               at_timed=None, flush=None):
     """Drive n_warm + n_timed chunks; returns, per timed chunk, (chunk ms, ms of
     the S denoising passes, ms of the KV-update pass).  force_every = P > 0
     computes every block of the denoising passes of chunks n with n % P == 0
     (the paper's periodic whole-generation refresh); per_chunk, a list, then
-    receives each chunk's skip count (the stream is synchronised per chunk)."""
+    receives each chunk's skip count (the stream is synchronised per chunk).
+    at_timed(xc) is called once, synchronised, before the first timed chunk;
+    flush(), when given, is enqueued before every timed pass (outside the
+    chunk's events it is not: use it only for per-kernel timings)."""
     L, C = m.tokens, m.hidden
     taus = synth.timesteps(m)
     x = torch.empty((L, C), dtype=torch.float32, device="cuda")
@@ -96,6 +107,8 @@ def run_stream(xc, m, eps_dev, actions, n_warm, n_timed, torch, profile=False, f
         timed = n >= n_warm
         if timed and n == n_warm:
             torch.cuda.synchronize()
+            if at_timed is not None:
+                at_timed(xc)
             if profile:
                 xc.profile(True)
         if timed:
@@ -104,6 +117,8 @@ def run_stream(xc, m, eps_dev, actions, n_warm, n_timed, torch, profile=False, f
         x.copy_(eps)
         fl = xcp_force_full if force_every and n % force_every == 0 else 0
         for t in range(m.n_steps):
+            if flush is not None and timed:
+                flush()
             xc.forward_chunk(t, taus[t], actions[n], x, y, fl)
             if t + 1 < m.n_steps:
                 sg = synth.sampler_sigma(m, t + 1)
@@ -170,6 +185,117 @@ def cpu_baseline(w, weights, seed):
                        f"{m.n_blocks * (m.n_steps + 1)} block evaluations to a full-compute chunk")}
 
 
+def gate_bytes(m, gate, xcp, folded):
+    """Algorithmic bytes of one gate-comparison launch: the cached fingerprint
+    read and the current one written, the spatial rows gathered, and the
+    global channel's source (one read of the block input, or the previous
+    block's MLP-down column-sum partials)."""
+    L, C = m.tokens, m.hidden
+    n_srows = len(xcp.xc_fingerprint_rows(m, gate))
+    fp_rows = n_srows + sum(g.views for g in m.groups)
+    if folded:
+        return 4.0 * n_srows * C + 8.0 * fp_rows * C + 16.0 * ((L + 31) // 32) * C
+    return 4.0 * L * C + 8.0 * fp_rows * C
+
+
+def skip_path(w, m, eps_dev, actions, make_xc, n_timed, torch, xcp):
+    """Every gated block skips: no anchor, fixed cosine threshold -1 and no
+    deviation bound.  After the warmup chunk each denoising pass is the
+    conditioning plus B skipped blocks (gate comparison, decision, the
+    skip-add inside the first LayerNorm launch, and the block's other
+    launches returning at entry).  Reports the per-skipped-block time from
+    pass events and the per-launch averages of one more chunk's passes."""
+    g = synth.with_gate(w, front_anchors=0, back_anchors=0, adaptive=0, tau_cos_fixed=-1.0, tau_dev=math.inf).gate
+    xc = make_xc(g)
+    L, C = m.tokens, m.hidden
+    taus = synth.timesteps(m)
+    x = torch.empty((L, C), dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    pass_ms = []
+    n_all = 1 + n_timed + 1
+    for n in range(n_all):
+        x.copy_(eps_dev[n])
+        last = n == n_all - 1
+        if last:
+            torch.cuda.synchronize()
+            xc.profile(True)
+        for t in range(m.n_steps):
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            ev[0].record()
+            xc.forward_chunk(t, taus[t], actions[n], x, y)
+            ev[1].record()
+            if 1 <= n < n_all - 1:
+                pass_ms.append(ev)
+            if t + 1 < m.n_steps:
+                sg = synth.sampler_sigma(m, t + 1)
+                xc.axpby(1.0 - sg, y, sg, eps_dev[n], x, L * C)
+        if last:
+            torch.cuda.synchronize()
+            xc.profile(False)
+        xc.kv_update(synth.KV_UPDATE_TIMESTEP, actions[n], y, None)
+    torch.cuda.synchronize()
+    kt = kernel_table(xc, xcp)
+    st = xc.stats()
+    xc.close()
+    ms = [e[0].elapsed_time(e[1]) for e in pass_ms]
+    per_block_us = 1e3 * statistics.mean(ms) / m.n_blocks
+    kernels = {}
+    folded = m.dtype == synth.BF16 and min(gr.frames * gr.height * gr.width for gr in m.groups) >= 32
+    for k, v in kt.items():
+        e = {"launches": v["launches"], "avg_us": round(v["avg_us"], 2)}
+        if k == "skip_add":
+            e["bytes"] = 10.0 * L * C if m.dtype == synth.BF16 else 12.0 * L * C
+            e["gbs"] = round(e["bytes"] / (v["avg_us"] * 1e-6) / 1e9, 1)
+            e["hbm_frac"] = round(e["gbs"] / PEAK_HBM_GBS, 4)
+        if k == "gate":
+            # block 0 reads its input; the others take the previous block's sums
+            b_all = gate_bytes(m, g, xcp, False) + (m.n_blocks - 1) * gate_bytes(m, g, xcp, folded)
+            e["bytes_mean"] = b_all / m.n_blocks
+            e["gbs"] = round(e["bytes_mean"] / (v["avg_us"] * 1e-6) / 1e9, 1)
+        kernels[k] = e
+    return {"pass_ms_mean": round(statistics.mean(ms), 3), "per_skipped_block_us": round(per_block_us, 2),
+            "skips": st["skips"], "kernels": kernels,
+            "note": "every gated block skipped (no anchor, cosine threshold -1): a pass = conditioning + "
+                    f"{m.n_blocks} skipped blocks; per-skipped-block time = pass time / blocks"}
+
+
+def cold_gate(w, m, eps_dev, actions, make_xc, torch, xcp, n_pass=8):
+    """The gate comparison that reads the block input (one gated block, no
+    anchor), timed per launch with the input in the last-level cache (the
+    previous launch wrote it) and after a 1 GiB write evicts it."""
+    wg = synth.with_gate(synth.with_model(w, n_blocks=1), front_anchors=0, adaptive=0, tau_cos_fixed=-1.0,
+                         tau_dev=math.inf)
+    m1 = wg.model
+    flush_buf = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    out = {}
+    for mode in ("in_stream", "cold"):
+        xc = xcp.XCache(m1, wg.gate, make_xc.weights[: synth.block_numel(m1)], make_xc.stream)
+        L, C = m1.tokens, m1.hidden
+        x = torch.empty((L, C), dtype=torch.float32, device="cuda")
+        y = torch.empty_like(x)
+        for n in range(2):
+            x.copy_(eps_dev[n])
+            if n == 1:
+                torch.cuda.synchronize()
+                xc.profile(True)
+            for i in range(n_pass if n == 1 else 1):
+                if n == 1 and mode == "cold":
+                    flush_buf.fill_(float(i))
+                xc.forward_chunk(0, 1000.0, actions[n], x, y)
+            if n == 1:
+                torch.cuda.synchronize()
+                xc.profile(False)
+            xc.kv_update(synth.KV_UPDATE_TIMESTEP, actions[n], y, None)
+        cnt, tot = xc.kernel_times(xcp.XC_KERN_GATE, clear=True)
+        xc.close()
+        b = gate_bytes(m1, wg.gate, xcp, False)
+        us = 1e3 * tot / cnt
+        out[mode] = {"launches": cnt, "avg_us": round(us, 2), "bytes": b, "gbs": round(b / (us * 1e-6) / 1e9, 1),
+                     "hbm_frac": round(b / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+    del flush_buf
+    return out
+
+
 def ablations(w, m, weights, eps_dev, actions, make_xc, args, torch):
     """Synthetic analogues of the paper's gate ablations (Section 4.4): the same stream under
     step-0 handling, anchor, staleness, refresh and threshold variants; skip rate and latency only."""
@@ -213,6 +339,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gate-off", action="store_true")
     ap.add_argument("--no-alt-tau", action="store_true", help="skip the extra gate-on run at tau_floor 0.95")
+    ap.add_argument("--no-stress", action="store_true", help="skip the gate-stress stream run")
     ap.add_argument("--force-every", type=int, default=0,
                     help="also run the gate-on stream with every P-th generation computed in full and report "
                          "the per-chunk skip fractions (the paper's periodic refresh cadence)")
@@ -265,6 +392,7 @@ def main():
         if cond is not None:
             xc.set_condition(cond)
         return xc
+    make_xc.weights, make_xc.stream = weights, stream
 
     if args.calib_copy_mib:
         n = args.calib_copy_mib * (1 << 20) // 4
@@ -280,31 +408,40 @@ def main():
         print(json.dumps(ablations(w, m, weights, eps_dev, actions, make_xc, args, torch)), flush=True)
         return
 
+    def timed_rate(st0, st):
+        """Skip rate over the timed chunks' denoising block evaluations."""
+        return (st["skips"] - st0["skips"]) / max(1, st["evals_post_warmup"] - st0["evals_post_warmup"])
+
     # 1. gate on
     xc = make_xc(w.gate)
-    on_split = run_stream(xc, m, eps_dev, actions, args.warmup, args.steps, torch)
+    st0 = {}
+    on_split = run_stream(xc, m, eps_dev, actions, args.warmup, args.steps, torch,
+                          at_timed=lambda h: st0.update(h.stats()))
     on_ms = [v[0] for v in on_split]
     st = xc.stats()
-    # 3. gate kernels (same handle, two more chunks continue the stream state)
-    xc.reset()
-    prof_chunks = min(n_chunks, 3)
-    run_stream(xc, m, eps_dev, actions, prof_chunks - 1, 1, torch, profile=True)
-    gate_k = kernel_table(xc, xcp)
     xc.close()
-    log(f"gate on: mean {statistics.mean(on_ms):.2f} ms/chunk, skips {st['skips']} / "
-        f"{st['evals_post_warmup']}")
+    log(f"gate on: mean {statistics.mean(on_ms):.2f} ms/chunk, timed skips {st['skips'] - st0['skips']} / "
+        f"{st['evals_post_warmup'] - st0['evals_post_warmup']}")
+
+    # 3. the skip path alone, and the gate comparison that reads its input, in-stream and cold
+    skp = skip_path(w, m, eps_dev, actions, make_xc, min(2, n_chunks - 2), torch, xcp)
+    log(f"skip path: {skp['per_skipped_block_us']} us per skipped block")
+    cgate = cold_gate(w, m, eps_dev, actions, make_xc, torch, xcp)
+    log(f"gate reading x: in-stream {cgate['in_stream']['avg_us']} us, cold {cgate['cold']['avg_us']} us")
 
     # 1b. the same stream at the other tau_floor the paper states (0.95 vs Table 1's 0.97)
     alt = None
     if args.tau_floor is None and not args.no_alt_tau:
         wa = synth.with_gate(w, tau_floor=0.95)
         xc = make_xc(wa.gate)
-        alt_ms = [v[0] for v in run_stream(xc, m, eps_dev, actions, args.warmup, args.steps, torch)]
+        sa0 = {}
+        alt_ms = [v[0] for v in run_stream(xc, m, eps_dev, actions, args.warmup, args.steps, torch,
+                                           at_timed=lambda h: sa0.update(h.stats()))]
         sa = xc.stats()
         xc.close()
         alt = {"tau_floor": 0.95, "value": round(statistics.mean(alt_ms), 3),
                "chunk_ms_median": round(statistics.median(alt_ms), 3),
-               "skip_rate": round(sa["skips"] / max(1, sa["evals_post_warmup"]), 4)}
+               "skip_rate": round(timed_rate(sa0, sa), 4)}
         log(f"tau_floor 0.95: mean {alt['value']:.2f} ms/chunk, skip rate {alt['skip_rate']:.3f}")
 
     # 1c. periodic whole-generation refresh: skip fraction per chunk
@@ -334,12 +471,33 @@ def main():
         xc.close()
         log(f"gate off: mean {statistics.mean(off_ms):.2f} ms/chunk")
 
+    # 4. the gate-stress stream on the same shapes (scene cut every 8th chunk, steering step every 5th)
+    stress = None
+    if args.workload == 2 and not args.rope and not args.cond_len and not args.no_stress:
+        ws = synth.workload(4)
+        n_s = args.warmup + args.steps
+        e_s = [torch.from_numpy(e).cuda() for e in synth.latent_stream(m, ws.stream, args.seed, n_s)]
+        a_s = list(synth.action_stream(m, ws.stream, args.seed, n_s))
+        xc = make_xc(ws.gate)
+        ss0 = {}
+        s_ms = [v[0] for v in run_stream(xc, m, e_s, a_s, args.warmup, args.steps, torch,
+                                         at_timed=lambda h: ss0.update(h.stats()))]
+        ss = xc.stats()
+        xc.close()
+        del e_s
+        stress = {"workload": ws.name, "value": round(statistics.mean(s_ms), 3),
+                  "chunk_ms_median": round(statistics.median(s_ms), 3), "skip_rate": round(timed_rate(ss0, ss), 4),
+                  "chunk_ms": [round(v, 2) for v in s_ms]}
+        if off_ms:
+            stress["speedup_vs_full_compute"] = round(statistics.mean(off_ms) / stress["value"], 3)
+        log(f"gate stress: mean {stress['value']:.2f} ms/chunk, skip rate {stress['skip_rate']:.3f}")
+
     Lk = m.kv_window * m.tokens  # every timed chunk sees the full window (warmup >= window - 1)
     steady = args.warmup >= m.kv_window - 1
     fl_block = block_flops(m, Lk)
     B, S = m.n_blocks, m.n_steps
     # skip rate over the timed chunks' denoising block evaluations (warmup chunks excluded)
-    skip_rate = st["skips"] / max(1, st["evals_post_warmup"])
+    skip_rate = timed_rate(st0, st)
     on_mean = statistics.mean(on_ms)
     res = {
         "metric": METRIC,
@@ -365,8 +523,8 @@ def main():
         "passes_ms_mean": round(statistics.mean(v[1] for v in on_split), 3),
         "kv_update_ms_mean": round(statistics.mean(v[2] for v in on_split), 3),
         "skip_rate": round(skip_rate, 4),
-        "skips": st["skips"],
-        "block_evals_post_warmup": st["evals_post_warmup"],
+        "skips_timed": st["skips"] - st0["skips"],
+        "block_evals_timed": st["evals_post_warmup"] - st0["evals_post_warmup"],
         # per (denoising step t, block b): skips over the whole stream, and the
         # gate's running cosine average s-bar after the last chunk
         "skip_counts_tb": np.asarray(st["skip_counts"]).reshape(S, B).astype(int).tolist(),
@@ -375,6 +533,10 @@ def main():
     }
     if alt:
         res["alt_tau_floor"] = alt
+    if stress:
+        res["gate_stress"] = stress
+    res["skip_path"] = skp
+    res["gate_reading_input"] = cgate
     if cadence:
         res["periodic_refresh"] = cadence
     if off_ms:
@@ -414,29 +576,6 @@ def main():
             if k == "ln_mod":
                 e["gbs"] = round(6.0 * m.tokens * m.hidden / (v["avg_us"] * 1e-6) / 1e9, 1)
             res["kernels_full_compute"][k] = e
-    gk = {}
-    L, C = m.tokens, m.hidden
-    for k, v in gate_k.items():
-        e = {"launches": v["launches"], "avg_us": round(v["avg_us"], 2)}
-        if k == "gate":
-            # the cached fingerprint read and the current one written, plus the
-            # global channel's source: one read of x, or (bf16 models whose
-            # cameras all have >= 32 tokens, every gated block but block 0)
-            # the MLP-down column-sum partials of the previous block
-            n_srows = len(xcp.xc_fingerprint_rows(m, w.gate))
-            fp_rows = n_srows + sum(g.views for g in m.groups)
-            folded = m.dtype == synth.BF16 and min(g.frames * g.height * g.width for g in m.groups) >= 32
-            n_rb = (L + 31) // 32
-            e["global_channel"] = "MLP-down column-sum partials" if folded else "one read of the block input"
-            e["bytes"] = (4.0 * n_srows * C + 8.0 * fp_rows * C + 16.0 * n_rb * C) if folded else \
-                (4.0 * L * C + 8.0 * fp_rows * C)
-            e["gbs"] = round(e["bytes"] / (v["avg_us"] * 1e-6) / 1e9, 1)
-            e["hbm_frac"] = round(e["gbs"] / PEAK_HBM_GBS, 4)
-        if k == "ln_mod":
-            e["note"] = ("the first LayerNorm launch of a gated evaluation writes x + r_hat when the block "
-                         "is skipped: averaged over LayerNorm, skip-path and return-at-entry launches")
-        gk[k] = e
-    res["kernels_gate_on"] = gk
     if not args.no_cpu_baseline:
         log("cpu baseline: one oracle block at full shape ...")
         res["cpu_baseline"] = cpu_baseline(w, weights, args.seed)

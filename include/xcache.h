@@ -318,10 +318,11 @@ xc_status xc_fingerprint_rows(const xc_model_config* model, const xc_gate_config
  * bracketed by HIP events on the bound stream.  A gated evaluation is two
  * launches: XC_KERN_GATE reads the block input once, forms the fingerprint
  * and compares it with the cached one; XC_KERN_GATE_DECIDE takes the
- * decision.  The skip path (Eq. 4) runs inside the block's first
- * XC_KERN_LN_MOD launch, which writes x + rhat when the block is skipped and
- * the LayerNorm otherwise; XC_KERN_SKIP_ADD is kept for numbering and counts
- * no launches.  The cross-attention layer's kernels are XC_KERN_CROSS_Q (its
+ * decision.  The skip path (Eq. 4) runs inside the block's first LayerNorm
+ * launch: for a block whose gate was evaluated that launch is counted as
+ * XC_KERN_SKIP_ADD (it writes x + rhat when the block is skipped and the
+ * LayerNorm otherwise); every other LayerNorm launch is XC_KERN_LN_MOD.  The
+ * cross-attention layer's kernels are XC_KERN_CROSS_Q (its
  * LayerNorm and q projection), XC_KERN_CROSS_ATTENTION and XC_KERN_CROSS_O
  * (output projection and residual). */
 enum {

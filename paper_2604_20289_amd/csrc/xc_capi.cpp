@@ -516,7 +516,7 @@ void compute_block(xc_handle* h, int b, const float* x, float* out, const int* f
   void* vt_b = wptr<void>(h->vt, (size_t)b * H * h->Lcap * D, esz);
   {
     // a skipped block's output x + rhat is written by this launch (Eq. 4)
-    Prof p(h, XC_KERN_LN_MOD);
+    Prof p(h, flag ? XC_KERN_SKIP_ADD : XC_KERN_LN_MOD);
     launch_ln_mod(h->dtype, x, shift1, scale1, h->hbuf, L, C, flag, h->st, flag ? rhat_tb : nullptr,
                   flag ? out : nullptr);
   }
