@@ -119,6 +119,63 @@ __global__ __launch_bounds__(256) void adaln_kernel(const T* __restrict__ w, con
   }
 }
 
+// The same GEMV when a row of W_ada is a whole number of 16-byte chunks (every
+// supported conditioning width): the weights of all blocks form one
+// contiguous [rows][dc] matrix, and a wave takes 32 consecutive rows, i.e.
+// one contiguous span of 32 * cpr chunks, walked lane-linearly (every load
+// instruction reads 1 KB of consecutive bytes).  Each chunk's dot product with
+// its slice of SiLU(c) goes to LDS; lane r < 32 then sums row r's cpr
+// partials in order (deterministic).
+template <typename T>
+__global__ __launch_bounds__(256) void adaln_flat_kernel(const T* __restrict__ w, const float* __restrict__ b,
+                                                         const float* __restrict__ cond_silu, int n_rows, int dc,
+                                                         float* __restrict__ mod) {
+  constexpr int V = 16 / sizeof(T);
+  constexpr int kRows = 32;   // rows per wave
+  constexpr int kBatch = 8;   // chunk loads in flight per lane
+  typedef T tvec __attribute__((ext_vector_type(V)));
+  __shared__ float s_c[kMaxCond];
+  extern __shared__ float s_part[];  // [4 waves][kRows * cpr]
+  for (int j = threadIdx.x; j < dc; j += blockDim.x) s_c[j] = cond_silu[j];
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int cpr = dc / V;  // chunks per row
+  const long long row0 = ((long long)blockIdx.x * 4 + wave) * kRows;
+  if (row0 >= n_rows) return;
+  const int rows = (int)min((long long)kRows, n_rows - row0);
+  const int n_chunks = rows * cpr;
+  const tvec* src = reinterpret_cast<const tvec*>(w + row0 * dc);
+  float* part = s_part + wave * kRows * cpr;
+  for (int c0 = 0; c0 < n_chunks; c0 += 64 * kBatch) {
+    tvec v[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int c = c0 + u * 64 + lane;
+      if (c < n_chunks) v[u] = src[c];
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int c = c0 + u * 64 + lane;
+      if (c < n_chunks) {
+        const int k = c % cpr;
+        float acc = 0.f;
+#pragma unroll
+        for (int e = 0; e < V; ++e) acc += to_f(v[u][e]) * s_c[k * V + e];
+        part[c] = acc;
+      }
+    }
+  }
+  // lanes read partials other lanes of this wave wrote: LDS operations of one
+  // wave complete in order, the fence keeps the compiler from reordering them
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  if (lane < rows) {
+    float a = 0.f;
+    for (int k = 0; k < cpr; ++k) a += part[lane * cpr + k];
+    mod[row0 + lane] = a + b[row0 + lane];
+  }
+}
+
 // h = LayerNorm(x) * (1 + scale) + shift per row (no affine, biased variance,
 // eps 1e-6), one wave per row, values held in registers between the passes.
 // With a skip flag that is set the block is skipped: the kernel then writes
@@ -346,6 +403,16 @@ void launch_adaln(int dtype, const void* w_ada, const float* b_ada, const float*
   // W_ada is [n_blocks][rows_per_block][dc] and b_ada [n_blocks][rows_per_block]:
   // block_stride_w = rows_per_block * dc, the bias stride is rows_per_block.
   int total = rows_per_block * n_blocks;
+  const int esz = dtype == 1 ? 2 : 4;
+  if ((dc * esz) % 16 == 0 && block_stride_w == (long long)rows_per_block * dc) {
+    const int grid = (total + 127) / 128;  // 4 waves x 32 rows
+    const size_t lds = (size_t)4 * 32 * (dc * esz / 16) * sizeof(float);
+    if (dtype == 1)
+      adaln_flat_kernel<bf16><<<grid, 256, lds, st>>>((const bf16*)w_ada, b_ada, cond_silu, total, dc, mod);
+    else
+      adaln_flat_kernel<float><<<grid, 256, lds, st>>>((const float*)w_ada, b_ada, cond_silu, total, dc, mod);
+    return;
+  }
   int grid = (total + 31) / 32;  // 4 waves x 8 rows
   if (dtype == 1)
     adaln_kernel<bf16><<<grid, 256, 0, st>>>((const bf16*)w_ada, b_ada, cond_silu, rows_per_block, block_stride_w,

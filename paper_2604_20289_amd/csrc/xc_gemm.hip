@@ -7,10 +7,11 @@
 // weights [out][in]), so a lane's MFMA operand is one 16-byte LDS read, and
 // stage tiles go from global memory straight into LDS (global_load_lds).
 //  * gemm_bf16_kernel: (64*MT) x 128 tiles, two workgroups per CU; used for
-//    the fused QKV projection and for widths that are not multiples of 192.
+//    the fused QKV projection, the MLP-up projection and for widths that are
+//    not multiples of 192.
 //  * gemm_bf16_persistent: 256 x 192 tiles, one persistent workgroup per CU
-//    streaming its tiles through a 4-deep LDS ring; used for the other
-//    projections.
+//    streaming its tiles through a 4-deep LDS ring; used for the output and
+//    MLP-down projections.
 // Both run the element-wise epilogues through tile_epilogue (software-
 // pipelined operand loads, range-checked buffer stores).
 //
@@ -850,7 +851,10 @@ template <int MODE>
 void launch_mode(int dtype, const void* A, const void* W, int M, int N, int K, const EpiArgs& e, const int* flag,
                  hipStream_t st) {
   if (dtype == 1) {
-    if constexpr (MODE != EPI_QKV) {
+    // the MLP-up product runs faster on the two-workgroup kernel (measured at
+    // the multi-camera shape: 158-164 us against 175-177 us for 256 x 192
+    // persistent tiles, whose 896 tiles make 3.5 rounds on 256 CUs)
+    if constexpr (MODE != EPI_QKV && MODE != EPI_UP) {
       if (use_persistent(N, K)) {
         launch_persistent<MODE, 3>(A, W, M, N, K, e, flag, st);
         return;
