@@ -351,6 +351,10 @@ def main():
                     help="model with the 3-D rotary embedding of the self-attention queries and keys")
     ap.add_argument("--cond-len", type=int, default=0,
                     help="model with a cross-attention layer over this many condition tokens")
+    ap.add_argument("--phase", choices=["full", "skip", "gate-cold"], default=None,
+                    help="run one phase alone and print its own JSON line (for profiling): 'full' = the gate-off "
+                         "stream (every block computed), 'skip' = the skip path (every gated block skipped), "
+                         "'gate-cold' = the gate comparison reading its input, in-stream and after a cache flush")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="copy a buffer of this many MiB once (calibrates rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     args = ap.parse_args()
@@ -406,6 +410,22 @@ def main():
 
     if args.ablations:
         print(json.dumps(ablations(w, m, weights, eps_dev, actions, make_xc, args, torch)), flush=True)
+        return
+    if args.phase == "full":
+        xc = make_xc(synth.with_gate(w, enabled=0).gate)
+        ms = [v[0] for v in run_stream(xc, m, eps_dev, actions, args.warmup, args.steps, torch)]
+        xc.close()
+        print(json.dumps({"phase": "full", "workload": w.name, "warmup": args.warmup, "steps": args.steps,
+                          "chunk_ms": [round(v, 3) for v in ms]}), flush=True)
+        return
+    if args.phase == "skip":
+        print(json.dumps({"phase": "skip", "workload": w.name,
+                          **skip_path(w, m, eps_dev, actions, make_xc, max(1, min(args.steps, n_chunks - 2)), torch,
+                                      xcp)}), flush=True)
+        return
+    if args.phase == "gate-cold":
+        print(json.dumps({"phase": "gate-cold", "workload": w.name,
+                          **cold_gate(w, m, eps_dev, actions, make_xc, torch, xcp)}), flush=True)
         return
 
     def timed_rate(st0, st):
