@@ -13,10 +13,24 @@ namespace xc {
 
 namespace {
 
+// Sum over the 64 lanes of a wave without LDS round trips: lane pairs and quads by DPP quad
+// permutations, quad pairs and 8-lane halves by the DPP row mirrors, then the
+// row pairs and the two half-waves by the permlane swaps.  Every step adds
+// two values that the partner lane adds in the other order, so every lane
+// ends with the same total, in the same order in every run.
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-  return v;
+  v += dpp_move<0xB1>(v);    // quad_perm [1,0,3,2]: lane ^ 1
+  v += dpp_move<0x4E>(v);    // quad_perm [2,3,0,1]: lane ^ 2
+  v += dpp_move<0x141>(v);   // row_half_mirror: quad 0 <-> quad 1 of each 8 lanes
+  v += dpp_move<0x140>(v);   // row_mirror: the two 8-lane halves of each row
+  const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(r16[0]) + __uint_as_float(r16[1]);
+  const auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r32[0]) + __uint_as_float(r32[1]);
 }
 
 template <typename T>
