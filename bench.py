@@ -55,8 +55,8 @@ PEAK_HBM_GBS = 8000.0
 # scaled by a 512 MiB copy-kernel calibration; valid only for the kernel
 # source they were taken on (sha1 prefix of the file).
 MEASURED_TRAFFIC = {
-    "attention": {"source": "paper_2604_20289_amd/csrc/xc_attention.hip", "sha1": "fb0e43f08a8bac04",
-                  "bytes": (358.8 + 89.7) * 1e6},
+    "attention": {"source": "paper_2604_20289_amd/csrc/xc_attention.hip", "sha1": "c40848a0aa57cc2b",
+                  "bytes": (359.9 + 88.6) * 1e6},
 }
 
 
@@ -596,6 +596,16 @@ def main():
             if k == "ln_mod":
                 e["gbs"] = round(6.0 * m.tokens * m.hidden / (v["avg_us"] * 1e-6) / 1e9, 1)
             res["kernels_full_compute"][k] = e
+    # the MFMA rate a register-only loop sustains on random bf16 operands: the
+    # practical ceiling the contraction kernels above can be read against
+    # (context only; roofline.peak stays the published dense figure)
+    ceil32 = xcp.xc_mfma_rate(0, True, torch.cuda.current_stream().cuda_stream)
+    ceil16 = xcp.xc_mfma_rate(1, True, torch.cuda.current_stream().cuda_stream)
+    res["mfma_ceiling"] = {"unit": "TFLOP/s", "operands": "random bf16",
+                           "mfma_32x32x16": round(ceil32, 1), "mfma_16x16x32": round(ceil16, 1)}
+    if "roofline" in res and ceil32 > 0:
+        res["mfma_ceiling"]["attention_frac_of_32x32x16"] = round(res["roofline"]["achieved"] / ceil32, 4)
+    log(f"mfma ceiling: {ceil32:.0f} TFLOP/s (32x32x16), {ceil16:.0f} TFLOP/s (16x16x32), random operands")
     if not args.no_cpu_baseline:
         log("cpu baseline: one oracle block at full shape ...")
         res["cpu_baseline"] = cpu_baseline(w, weights, args.seed)

@@ -25,6 +25,7 @@ SOURCES = [
     "xc_gate.hip",
     "xc_gemm.hip",
     "xc_attention.hip",
+    "xc_diag.hip",
     "xc_capi.cpp",
 ]
 

@@ -191,5 +191,8 @@ void launch_fill_f32(float* p, float v, long long n, hipStream_t st);
 // or [H][D][Lcap] (transposed = 1), rows 0 .. R-1
 void launch_read_cache(int dtype, const void* src, float* out, int H, int R, int D, long long Lcap, int transposed,
                        hipStream_t st);
+// Register-only MFMA loop (shape 0: 32x32x16, 1: 16x16x32 bf16), timed with
+// events on st; waits for it.
+hipError_t mfma_rate(int shape, int random, hipStream_t st, double* tflops);
 
 }  // namespace xc

@@ -36,7 +36,8 @@ KERNEL_NAMES = ["attention", "gemm_qkv", "gemm_oproj", "gemm_up", "gemm_down", "
 
 EXPORTED = ["xc_status_string", "xc_init", "xc_forward_chunk", "xc_forward_chunk_noalloc", "xc_kv_update",
             "xc_set_condition", "xc_read_cache", "xc_stats",
-            "xc_reset", "xc_destroy", "xc_axpby", "xc_fingerprint_rows", "xc_profile", "xc_kernel_times"]
+            "xc_reset", "xc_destroy", "xc_axpby", "xc_fingerprint_rows", "xc_profile", "xc_kernel_times",
+            "xc_mfma_rate"]
 
 
 class ViewGroupC(ctypes.Structure):
@@ -105,6 +106,7 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
         "xc_fingerprint_rows": (i32, [P(ModelConfigC), P(GateConfigC), vp, sz, P(sz)]),
         "xc_profile": (i32, [vp, i32]),
         "xc_kernel_times": (i32, [vp, i32, P(ctypes.c_int64), P(ctypes.c_double), i32]),
+        "xc_mfma_rate": (i32, [i32, i32, vp, P(ctypes.c_double)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -254,6 +256,14 @@ def xc_kernel_times(h: int, kind: int, clear: bool = False):
     _check(load_library().xc_kernel_times(h, kind, ctypes.byref(n), ctypes.byref(ms), 1 if clear else 0),
            "xc_kernel_times")
     return n.value, ms.value
+
+
+def xc_mfma_rate(shape: int, random_operands: bool, stream: Optional[int] = None) -> float:
+    """TFLOP/s of the register-only bf16 MFMA loop (shape 0: 32x32x16, 1: 16x16x32)."""
+    t = ctypes.c_double()
+    _check(load_library().xc_mfma_rate(shape, 1 if random_operands else 0, stream or None, ctypes.byref(t)),
+           "xc_mfma_rate")
+    return t.value
 
 
 class XCache:
