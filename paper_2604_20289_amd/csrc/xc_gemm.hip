@@ -230,14 +230,193 @@ struct GemmTile {
 
 __device__ __forceinline__ int swz32(int row, int c) { return row * GBK + ((c ^ ((row >> 2) & 3)) << 3); }
 
-// LDS bytes of the QKV epilogue: row sums of squares [BM][65] floats, reused
-// as the V^T transpose buffer [BN][BM + 8] bf16.
-template <int MT, int NT>
+// LDS bytes of the QKV epilogue: row sums of squares [BM][BN/NT + 5] floats,
+// reused as the V^T transpose buffer [BN][BM + 8] bf16.
+template <int BM, int BN, int NT>
 constexpr int qkv_epi_bytes() {
-  return GemmTile<MT, NT>::BM * 65 * 4 > GemmTile<MT, NT>::BN * (GemmTile<MT, NT>::BM + 8) * 2
-             ? GemmTile<MT, NT>::BM * 65 * 4
-             : GemmTile<MT, NT>::BN * (GemmTile<MT, NT>::BM + 8) * 2;
+  return BM * (BN / NT + 5) * 4 > BN * (BM + 8) * 2 ? BM * (BN / NT + 5) * 4 : BN * (BM + 8) * 2;
 }
+
+// QKV epilogue of a BM x BN tile (C = H*D columns per part, C % BN == 0, so a
+// tile lies in one of q, k, v): bias; for q and k the per-(row, head) RMSNorm
+// times the gain and the rotary embedding, stored bf16 to q_out / the key
+// cache; for v the transpose through LDS into the V^T cache.  The tile's
+// waves hold MT x NT accumulators each at rows wm*MT*32.., columns
+// wn*NT*32..; NTHR threads; lds holds qkv_epi_bytes<BM, BN, NT>() bytes.
+// accumulator element (mt, nt, g, r): tile row wm*MT*32 + mt*32 + g*8 + hi*4 + r,
+// tile column wn*NT*32 + nt*32 + lo
+template <int MT, int NT, int BM, int BN, int NTHR>
+__device__ __forceinline__ void qkv_epilogue(const EpiArgs& e, f32x16 (&acc)[MT][NT], char* lds, int m0, int n0,
+                                             int M, int wm, int wn, int tid, int hi, int lo) {
+  constexpr int NSLOT = BN / NT;  // column slots: (waves across N) x 32 lanes
+  constexpr int SS = NSLOT + 5;   // row stride of the sums: the slots, up to 4 head scales, odd
+  {
+    const int C = e.H * e.D;
+    const int lpart = n0 / C;            // a tile never straddles two column blocks
+    const int part = lpart + e.part_base;  // 0 q, 1 k, 2 v
+    const int head0 = (n0 - lpart * C) / e.D;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const float bv = e.bias[n0 + wn * NT * 32 + nt * 32 + lo];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[mt][nt][r] += bv;
+      }
+    if (part < 2) {
+      // per (row, head) RMS over the head's D columns: lane partials -> LDS
+      float* ss = reinterpret_cast<float*>(lds);  // [BM][SS]
+      const int slot = wn * 32 + lo;             // NSLOT column slots of NT columns' squares each
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            float p = 0.f;
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) p += acc[mt][nt][g * 4 + r] * acc[mt][nt][g * 4 + r];
+            ss[(wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r) * SS + slot] = p;
+          }
+      __syncthreads();
+      // heads per tile: BN / D; slots per head NSLOT / heads (a wave's columns lie in one head)
+      const int hpt = BN / e.D, sph = NSLOT / hpt;
+      for (int idx = tid; idx < BM * hpt; idx += NTHR) {
+        const int row = idx / hpt, hd = idx - row * hpt;
+        float sum = 0.f;
+        for (int j = 0; j < sph; ++j) sum += ss[row * SS + hd * sph + j];
+        ss[row * SS + NSLOT + hd] = 1.0f / sqrtf(sum / (float)e.D + 1e-6f);  // slots NSLOT + hd hold the scales
+      }
+      __syncthreads();
+      const float* gain = part == 0 ? e.gq : e.gk;
+      const bool rope = e.rope.tab != nullptr;
+      // rotary embedding, per column of this lane: the table entry of its pair
+      // at axis position 0, the entry stride per position, the position's bit
+      // offset in the packed row coordinates
+      int rbase[NT], rstride[NT], rshift[NT];
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const int tcol = wn * NT * 32 + nt * 32 + lo;
+        int pair = (tcol - (tcol / e.D) * e.D) >> 1, a = 0;
+        if (pair >= e.rope.np[0]) {
+          pair -= e.rope.np[0];
+          a = 1;
+          if (pair >= e.rope.np[1]) {
+            pair -= e.rope.np[1];
+            a = 2;
+          }
+        }
+        rbase[nt] = e.rope.off[a] + pair;
+        rstride[nt] = e.rope.np[a];
+        rshift[nt] = 10 * a;
+      }
+      // normalise (and rotate) in place first, store afterwards: no store sits
+      // between the table loads, whose waits would otherwise also wait for it
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          // the table entries of this group of 4 rows are loaded together (one wait, not one per value)
+          float2 cs[4][NT];
+          if (rope) {
+            int packed[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r)  // rows past M: clamped, never stored
+              packed[r] = e.rope.pos[min(m0 + wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r, M - 1)];
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+#pragma unroll
+              for (int nt = 0; nt < NT; ++nt)
+                cs[r][nt] = e.rope.tab[rbase[nt] + ((packed[r] >> rshift[nt]) & 1023) * rstride[nt]];
+          }
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int trow = wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r;
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+              const int tcol = wn * NT * 32 + nt * 32 + lo;
+              const int hd = tcol / e.D, dd = tcol - hd * e.D;
+              float v = acc[mt][nt][g * 4 + r] * ss[trow * SS + NSLOT + hd] * gain[dd];
+              if (rope) {
+                // rotary pair (dd & ~1, dd | 1) = lanes (lo & ~1, lo | 1) of the same row, swapped
+                // by a DPP quad permutation [1, 0, 3, 2]: (a, b) -> (a c - b s, a s + b c)
+                const float pv = __builtin_bit_cast(
+                    float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
+                v = v * cs[r][nt].x + ((lo & 1) ? pv : -pv) * cs[r][nt].y;
+              }
+              acc[mt][nt][g * 4 + r] = v;
+            }
+          }
+        }
+      // Stores: a wave's 32*NT columns lie in one head (NT*32 <= D), whose rows
+      // [m0, min(m0 + BM, M)) form one buffer range; the even lane of each
+      // column pair stores both values as one dword (the odd lane's offset is
+      // the range's end, so its store is dropped), and rows past M are dropped
+      // by the range check, so no branch separates the stores.
+      static_assert(NT * 32 <= 64, "one head per wave");
+      const int hd = (wn * NT * 32) / e.D;
+      const long long hh = head0 + hd;
+      const int rows = min(BM, M - m0);
+      bf16* hbase = part == 0 ? reinterpret_cast<bf16*>(e.q_out) + (hh * e.Mpad + m0) * e.D
+                              : reinterpret_cast<bf16*>(e.k_cache) + (hh * e.Lcap + e.kv_off + m0) * e.D;
+      const __amdgpu_buffer_rsrc_t dst = __builtin_amdgcn_make_buffer_rsrc(hbase, (short)0, rows * e.D * 2, 0x00020000);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int trow = wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r;
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+              const int dd = (wn * NT * 32 + nt * 32 + lo) - hd * e.D;
+              const float v = acc[mt][nt][g * 4 + r];
+              const float pv = __builtin_bit_cast(
+                  float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
+              const unsigned two = (unsigned)__builtin_bit_cast(unsigned short, (bf16)v) |
+                                   ((unsigned)__builtin_bit_cast(unsigned short, (bf16)pv) << 16);
+              const int off = (lo & 1) ? rows * e.D * 2 : (trow * e.D + dd) * 2;
+              __builtin_amdgcn_raw_buffer_store_b32(two, dst, off, 0, 0);
+            }
+          }
+    } else {
+      // V^T: transpose the tile through LDS, then write rows of consecutive tokens
+      bf16* vt = reinterpret_cast<bf16*>(lds);  // [BN][BM + 8]
+      constexpr int VS = BM + 8;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+          for (int g = 0; g < 4; ++g)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              vt[(wn * NT * 32 + nt * 32 + lo) * VS + wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r] =
+                  (bf16)acc[mt][nt][g * 4 + r];
+      __syncthreads();
+      const int rows = min(BM, M - m0);
+      for (int idx = tid; idx < BN * (BM / 2); idx += NTHR) {
+        const int col = idx / (BM / 2), rp = (idx - col * (BM / 2)) * 2;
+        if (rp >= rows) continue;
+        const int hd = col / e.D, dd = col - hd * e.D;
+        bf16* dst = reinterpret_cast<bf16*>(e.vt_cache) + ((long long)(head0 + hd) * e.D + dd) * e.Lcap + e.kv_off + m0 + rp;
+        if (rp + 1 < rows) {
+          typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+          bf16x2 two = {vt[col * VS + rp], vt[col * VS + rp + 1]};
+          if (((e.kv_off + m0 + rp) & 1) == 0) {
+            *reinterpret_cast<bf16x2*>(dst) = two;
+          } else {
+            dst[0] = two[0];
+            dst[1] = two[1];
+          }
+        } else {
+          dst[0] = vt[col * VS + rp];
+        }
+      }
+    }
+  }
+}
+
 
 template <int MODE, int MT, int NT>
 __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(const bf16* __restrict__ A, const bf16* __restrict__ W,
@@ -246,7 +425,7 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(const bf16* __restric
   if (flag != nullptr && *flag) return;
   typedef GemmTile<MT, NT> T;
   constexpr int MAIN_BYTES = 3 * T::STAGE * 2;
-  constexpr int EPI_BYTES = MODE == EPI_QKV ? qkv_epi_bytes<MT, NT>() : 0;
+  constexpr int EPI_BYTES = MODE == EPI_QKV ? qkv_epi_bytes<T::BM, T::BN, NT>() : 0;
   constexpr int LDS_BYTES = MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES;
   __shared__ __attribute__((aligned(16))) char lds[LDS_BYTES];
   bf16* sbuf = reinterpret_cast<bf16*>(lds);
@@ -347,171 +526,144 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(const bf16* __restric
   // accumulator element (mt, nt, g, r): tile row wm*MT*32 + mt*32 + g*8 + hi*4 + r,
   // tile column wn*NT*32 + nt*32 + lo
   if constexpr (MODE == EPI_QKV) {
-    const int C = e.H * e.D;
-    const int lpart = n0 / C;            // a tile never straddles two column blocks
-    const int part = lpart + e.part_base;  // 0 q, 1 k, 2 v
-    const int head0 = (n0 - lpart * C) / e.D;
+    qkv_epilogue<MT, NT, T::BM, T::BN, 256>(e, acc, lds, m0, n0, M, wm, wn, tid, hi, lo);
+  } else {
+    tile_epilogue<MODE, MT, NT>(e, acc, m0, wm * MT * 32 + hi * 4, n0 + wn * NT * 32 + lo, M, T::BM);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Wide bf16 MFMA GEMM: one workgroup of 8 waves per CU owns a 256 x 256 tile,
+// its waves in a 2 x 4 arrangement of 128 x 64 sub-tiles (4 x 2 accumulators
+// each, as in gemm_bf16_kernel).  Stages are 64 deep: every DMA request
+// fetches 128 contiguous bytes of a row (a whole cache line; 64-byte
+// requests, as in the 32-deep stages above, measured at 14 TB/s of global ->
+// LDS throughput against 22 TB/s for 128-byte ones), and per output element a
+// 256 x 256 tile moves a third fewer operand bytes than two 256 x 128 tiles.
+// Two 64 KB stages fit in LDS: the next stage is requested at the top of a
+// step, while the current one is multiplied.  LDS rows are 128 bytes with
+// their 16-byte chunks XOR-swizzled (swz8) so the 32 rows a half-wave reads
+// at one chunk position fall in distinct banks.  Used for the QKV and MLP-up
+// projections when N % 256 == 0 and K % 64 == 0 (and C % 256 == 0 for QKV).
+// ---------------------------------------------------------------------------
+constexpr int WBM = 256, WBN = 256, WBK = 64;
+constexpr int WSTAGE = (WBM + WBN) * WBK;  // bf16 elements per stage (64 KB)
+
+// physical 16-byte chunk of logical chunk c in a 128-byte LDS row r (an
+// involution in c): any 8 consecutive rows at distinct chunks, any 16 at
+// distinct (row parity, chunk) pairs
+__device__ __forceinline__ int swz8(int r, int c) { return c ^ ((r & 7) ^ ((r >> 3) & 1)); }
+
+// one 16-byte chunk per lane, global -> LDS; lane l lands at byte 16 l of the
+// wave's 1 KB block
+__device__ __forceinline__ void dma16(const bf16* src, bf16* lds_block) {
+  __builtin_amdgcn_global_load_lds(src, lds_block, 16, 0, 0);
+}
+
+template <int MODE>
+__global__ __launch_bounds__(512, 1) void gemm_bf16_wide(const bf16* __restrict__ A, const bf16* __restrict__ W,
+                                                         int M, int N, int K, EpiArgs e,
+                                                         const int* __restrict__ flag) {
+  if (flag != nullptr && *flag) return;
+  constexpr int MT = 4, NT = 2;
+  constexpr int MAIN_BYTES = 2 * WSTAGE * 2;
+  constexpr int EPI_BYTES = MODE == EPI_QKV ? qkv_epi_bytes<WBM, WBN, NT>() : 0;
+  constexpr int LDS_BYTES = MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES;
+  __shared__ __attribute__((aligned(1024))) char lds[LDS_BYTES];
+  bf16* sbuf = reinterpret_cast<bf16*>(lds);
+
+  const int n_tm = (M + WBM - 1) / WBM, n_tn = N / WBN;
+  const int total = n_tm * n_tn;
+  const int per_xcd = (total + kXcd - 1) / kXcd;
+  const int t = (blockIdx.x % kXcd) * per_xcd + blockIdx.x / kXcd;
+  if (t >= total) return;
+  constexpr int GM = 8;
+  const int in_group = GM * n_tn;
+  const int first_m = (t / in_group) * GM;
+  const int gm = min(GM, n_tm - first_m);
+  const int tm = first_m + (t % in_group) % gm, tn = (t % in_group) / gm;
+  const int m0 = tm * WBM, n0 = tn * WBN;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 2, wn = wave & 3;
+  const int hi = lane >> 5, lo = lane & 31;
+  const bf16* Ab = A + (long long)m0 * K;
+  const bf16* Wb = W + (long long)n0 * K;
+  // DMA request I (0..31) of an operand fills its rows 8I .. 8I+7 lane-
+  // linearly (lane l: row 8I + l/8, physical chunk l%8, which holds the
+  // logical chunk swz8(row, l%8)); wave w issues I = w + 8i, i = 0..3
+  int goff[4];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+  for (int i = 0; i < 4; ++i) {
+    const int row = (wave + 8 * i) * 8 + (lane >> 3);
+    goff[i] = row * K + swz8(row, lane & 7) * 8;
+  }
+  // fragment reads: row lo (plus multiples of 32), logical chunk 2 kk + hi;
+  // the swizzle depends on the row's low 4 bits only
+  int foff[4];
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const float bv = e.bias[n0 + wn * NT * 32 + nt * 32 + lo];
+  for (int kk = 0; kk < 4; ++kk) foff[kk] = lo * WBK + swz8(lo, 2 * kk + hi) * 8;
+  f32x16 acc[MT][NT];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[mt][nt][r] += bv;
-      }
-    if (part < 2) {
-      // per (row, head) RMS over the head's D columns: lane partials -> LDS
-      float* ss = reinterpret_cast<float*>(lds);  // [BM][65]
-      const int slot = wn * 32 + lo;             // 64 column slots of 2 columns' squares each
+  for (int i = 0; i < MT; ++i)
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+    for (int j = 0; j < NT; ++j)
 #pragma unroll
-        for (int g = 0; g < 4; ++g)
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int KT = K / WBK;
+  auto issue = [&](int kt, int buf) __attribute__((always_inline)) {
+    bf16* sa = sbuf + buf * WSTAGE;
+    bf16* sb = sa + WBM * WBK;
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            float p = 0.f;
+    for (int i = 0; i < 4; ++i) dma16(Ab + goff[i] + kt * WBK, sa + (wave + 8 * i) * 512);
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt) p += acc[mt][nt][g * 4 + r] * acc[mt][nt][g * 4 + r];
-            ss[(wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r) * 65 + slot] = p;
-          }
-      __syncthreads();
-      // heads per tile: 128 / D (1 for D = 128, 2 for D = 64); slots per head 64 / heads
-      const int hpt = T::BN / e.D, sph = 64 / hpt;
-      for (int idx = tid; idx < T::BM * hpt; idx += 256) {
-        const int row = idx / hpt, hd = idx - row * hpt;
-        float sum = 0.f;
-        for (int j = 0; j < sph; ++j) sum += ss[row * 65 + hd * sph + j];
-        ss[row * 65 + 64 - hd] = 1.0f / sqrtf(sum / (float)e.D + 1e-6f);  // slots 64, 63 hold the scales
-      }
-      __syncthreads();
-      const float* gain = part == 0 ? e.gq : e.gk;
-      const bool rope = e.rope.tab != nullptr;
-      // rotary embedding, per column of this lane: the table entry of its pair
-      // at axis position 0, the entry stride per position, the position's bit
-      // offset in the packed row coordinates
-      int rbase[NT], rstride[NT], rshift[NT];
+    for (int i = 0; i < 4; ++i) dma16(Wb + goff[i] + kt * WBK, sb + (wave + 8 * i) * 512);
+  };
+  auto compute = [&](int buf) __attribute__((always_inline)) {
+    const bf16* sa = sbuf + buf * WSTAGE + (wm * MT * 32) * WBK;
+    const bf16* sb = sbuf + buf * WSTAGE + WBM * WBK + (wn * NT * 32) * WBK;
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int tcol = wn * NT * 32 + nt * 32 + lo;
-        int pair = (tcol - (tcol / e.D) * e.D) >> 1, a = 0;
-        if (pair >= e.rope.np[0]) {
-          pair -= e.rope.np[0];
-          a = 1;
-          if (pair >= e.rope.np[1]) {
-            pair -= e.rope.np[1];
-            a = 2;
-          }
-        }
-        rbase[nt] = e.rope.off[a] + pair;
-        rstride[nt] = e.rope.np[a];
-        rshift[nt] = 10 * a;
-      }
-      // normalise (and rotate) in place first, store afterwards: no store sits
-      // between the table loads, whose waits would otherwise also wait for it
+    for (int kk = 0; kk < WBK / 16; ++kk) {
+      bf16x8 a[MT], b[NT];
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+      for (int mt = 0; mt < MT; ++mt) a[mt] = *reinterpret_cast<const bf16x8*>(sa + mt * 32 * WBK + foff[kk]);
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          // the table entries of this group of 4 rows are loaded together (one wait, not one per value)
-          float2 cs[4][NT];
-          if (rope) {
-            int packed[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r)  // rows past M: clamped, never stored
-              packed[r] = e.rope.pos[min(m0 + wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r, M - 1)];
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-#pragma unroll
-              for (int nt = 0; nt < NT; ++nt)
-                cs[r][nt] = e.rope.tab[rbase[nt] + ((packed[r] >> rshift[nt]) & 1023) * rstride[nt]];
-          }
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int trow = wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r;
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) {
-              const int tcol = wn * NT * 32 + nt * 32 + lo;
-              const int hd = tcol / e.D, dd = tcol - hd * e.D;
-              float v = acc[mt][nt][g * 4 + r] * ss[trow * 65 + 64 - hd] * gain[dd];
-              if (rope) {
-                // rotary pair (dd & ~1, dd | 1) = lanes (lo & ~1, lo | 1) of the same row, swapped
-                // by a DPP quad permutation [1, 0, 3, 2]: (a, b) -> (a c - b s, a s + b c)
-                const float pv = __builtin_bit_cast(
-                    float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
-                v = v * cs[r][nt].x + ((lo & 1) ? pv : -pv) * cs[r][nt].y;
-              }
-              acc[mt][nt][g * 4 + r] = v;
-            }
-          }
-        }
-      // Stores: a wave's 32*NT columns lie in one head (NT*32 <= D), whose rows
-      // [m0, min(m0 + BM, M)) form one buffer range; the even lane of each
-      // column pair stores both values as one dword (the odd lane's offset is
-      // the range's end, so its store is dropped), and rows past M are dropped
-      // by the range check, so no branch separates the stores.
-      static_assert(NT * 32 <= 64, "one head per wave");
-      const int hd = (wn * NT * 32) / e.D;
-      const long long hh = head0 + hd;
-      const int rows = min(T::BM, M - m0);
-      bf16* hbase = part == 0 ? reinterpret_cast<bf16*>(e.q_out) + (hh * e.Mpad + m0) * e.D
-                              : reinterpret_cast<bf16*>(e.k_cache) + (hh * e.Lcap + e.kv_off + m0) * e.D;
-      const __amdgpu_buffer_rsrc_t dst = __builtin_amdgcn_make_buffer_rsrc(hbase, (short)0, rows * e.D * 2, 0x00020000);
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int g = 0; g < 4; ++g)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int trow = wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r;
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) {
-              const int dd = (wn * NT * 32 + nt * 32 + lo) - hd * e.D;
-              const float v = acc[mt][nt][g * 4 + r];
-              const float pv = __builtin_bit_cast(
-                  float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
-              const unsigned two = (unsigned)__builtin_bit_cast(unsigned short, (bf16)v) |
-                                   ((unsigned)__builtin_bit_cast(unsigned short, (bf16)pv) << 16);
-              const int off = (lo & 1) ? rows * e.D * 2 : (trow * e.D + dd) * 2;
-              __builtin_amdgcn_raw_buffer_store_b32(two, dst, off, 0, 0);
-            }
-          }
-    } else {
-      // V^T: transpose the tile through LDS, then write rows of consecutive tokens
-      bf16* vt = reinterpret_cast<bf16*>(lds);  // [BN][BM + 8]
-      constexpr int VS = T::BM + 8;
+      for (int nt = 0; nt < NT; ++nt) b[nt] = *reinterpret_cast<const bf16x8*>(sb + nt * 32 * WBK + foff[kk]);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-          for (int g = 0; g < 4; ++g)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-              vt[(wn * NT * 32 + nt * 32 + lo) * VS + wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r] =
-                  (bf16)acc[mt][nt][g * 4 + r];
-      __syncthreads();
-      const int rows = min(T::BM, M - m0);
-      for (int idx = tid; idx < T::BN * (T::BM / 2); idx += 256) {
-        const int col = idx / (T::BM / 2), rp = (idx - col * (T::BM / 2)) * 2;
-        if (rp >= rows) continue;
-        const int hd = col / e.D, dd = col - hd * e.D;
-        bf16* dst = reinterpret_cast<bf16*>(e.vt_cache) + ((long long)(head0 + hd) * e.D + dd) * e.Lcap + e.kv_off + m0 + rp;
-        if (rp + 1 < rows) {
-          typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-          bf16x2 two = {vt[col * VS + rp], vt[col * VS + rp + 1]};
-          if (((e.kv_off + m0 + rp) & 1) == 0) {
-            *reinterpret_cast<bf16x2*>(dst) = two;
-          } else {
-            dst[0] = two[0];
-            dst[1] = two[1];
-          }
-        } else {
-          dst[0] = vt[col * VS + rp];
-        }
-      }
+          acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mt], b[nt], acc[mt][nt], 0, 0, 0);
     }
+  };
+  // vmcnt(0) with the other counters left at their maximum (gfx9 encoding)
+#define XC_WAIT_VMCNT0() __builtin_amdgcn_s_waitcnt(0x3f70)
+  // stage k lives in buffer k mod 2; stage k+1 is requested at the top of
+  // step k (its buffer was released by the barrier that ended step k-1) and
+  // waited for at the bottom
+  issue(0, 0);
+  XC_WAIT_VMCNT0();
+  __syncthreads();
+  auto step = [&](int kt, int b0) __attribute__((always_inline)) {
+    if (kt + 1 < KT) issue(kt + 1, b0 ^ 1);
+    compute(b0);
+    XC_WAIT_VMCNT0();
+    __syncthreads();
+  };
+  int kt = 0;
+  for (; kt + 1 < KT; kt += 2) {
+    step(kt, 0);
+    step(kt + 1, 1);
+  }
+  if (kt < KT) step(kt, 0);
+#undef XC_WAIT_VMCNT0
+
+  if constexpr (MODE == EPI_QKV) {
+    qkv_epilogue<MT, NT, WBM, WBN, 512>(e, acc, lds, m0, n0, M, wm, wn, tid, hi, lo);
   } else {
-    tile_epilogue<MODE, MT, NT>(e, acc, m0, wm * MT * 32 + hi * 4, n0 + wn * NT * 32 + lo, M, T::BM);
+    tile_epilogue<MODE, MT, NT>(e, acc, m0, wm * MT * 32 + hi * 4, n0 + wn * NT * 32 + lo, M, WBM);
   }
 }
 
@@ -848,9 +1000,26 @@ void launch_bf16(const void* A, const void* W, int M, int N, int K, const EpiArg
 }
 
 template <int MODE>
+void launch_wide(const void* A, const void* W, int M, int N, int K, const EpiArgs& e, const int* flag,
+                 hipStream_t st) {
+  const int tiles = ((M + WBM - 1) / WBM) * (N / WBN);
+  const int grid = (tiles + kXcd - 1) / kXcd * kXcd;
+  gemm_bf16_wide<MODE><<<grid, 512, 0, st>>>((const bf16*)A, (const bf16*)W, M, N, K, e, flag);
+}
+
+template <int MODE>
 void launch_mode(int dtype, const void* A, const void* W, int M, int N, int K, const EpiArgs& e, const int* flag,
                  hipStream_t st) {
   if (dtype == 1) {
+    // the QKV and MLP-up products on the wide kernel (measured at the
+    // multi-camera shapes: 115 us against 140 us for QKV, 156 us against
+    // 190 us for MLP-up, on the two-workgroup kernel)
+    if constexpr (MODE == EPI_QKV || MODE == EPI_UP) {
+      if (N % WBN == 0 && K % WBK == 0 && (MODE != EPI_QKV || (e.H * e.D) % WBN == 0)) {
+        launch_wide<MODE>(A, W, M, N, K, e, flag, st);
+        return;
+      }
+    }
     // the MLP-up product runs faster on the two-workgroup kernel (measured at
     // the multi-camera shape: 158-164 us against 175-177 us for 256 x 192
     // persistent tiles, whose 896 tiles make 3.5 rounds on 256 CUs)
