@@ -533,9 +533,10 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(const bf16* __restric
 }
 
 // ---------------------------------------------------------------------------
-// Wide bf16 MFMA GEMM: one workgroup of 8 waves per CU owns a 256 x 256 tile,
-// its waves in a 2 x 4 arrangement of 128 x 64 sub-tiles (4 x 2 accumulators
-// each, as in gemm_bf16_kernel).  Stages are 64 deep: every DMA request
+// Wide bf16 MFMA GEMM: one workgroup of 8 waves per CU owns a 256 x BN tile,
+// its waves in a WMW x (8 / WMW) arrangement: 256 x 256 tiles as 2 x 4 waves
+// of 128 x 64 (4 x 2 accumulators each, as in gemm_bf16_kernel), 256 x 192
+// tiles as 4 x 2 waves of 64 x 96 (2 x 3).  Stages are 64 deep: every DMA request
 // fetches 128 contiguous bytes of a row (a whole cache line; 64-byte
 // requests, as in the 32-deep stages above, measured at 14 TB/s of global ->
 // LDS throughput against 22 TB/s for 128-byte ones), and per output element a
@@ -543,11 +544,11 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(const bf16* __restric
 // Two 64 KB stages fit in LDS: the next stage is requested at the top of a
 // step, while the current one is multiplied.  LDS rows are 128 bytes with
 // their 16-byte chunks XOR-swizzled (swz8) so the 32 rows a half-wave reads
-// at one chunk position fall in distinct banks.  Used for the QKV and MLP-up
-// projections when N % 256 == 0 and K % 64 == 0 (and C % 256 == 0 for QKV).
+// at one chunk position fall in distinct banks.  256 x 256 tiles serve the
+// QKV and MLP-up projections (N % 256 == 0, K % 64 == 0, and C % 256 == 0 for
+// QKV).
 // ---------------------------------------------------------------------------
-constexpr int WBM = 256, WBN = 256, WBK = 64;
-constexpr int WSTAGE = (WBM + WBN) * WBK;  // bf16 elements per stage (64 KB)
+constexpr int WBM = 256, WBK = 64;
 
 // physical 16-byte chunk of logical chunk c in a 128-byte LDS row r (an
 // involution in c): any 8 consecutive rows at distinct chunks, any 16 at
@@ -560,19 +561,21 @@ __device__ __forceinline__ void dma16(const bf16* src, bf16* lds_block) {
   __builtin_amdgcn_global_load_lds(src, lds_block, 16, 0, 0);
 }
 
-template <int MODE>
+template <int MODE, int BN, int WMW>
 __global__ __launch_bounds__(512, 1) void gemm_bf16_wide(const bf16* __restrict__ A, const bf16* __restrict__ W,
                                                          int M, int N, int K, EpiArgs e,
                                                          const int* __restrict__ flag) {
   if (flag != nullptr && *flag) return;
-  constexpr int MT = 4, NT = 2;
-  constexpr int MAIN_BYTES = 2 * WSTAGE * 2;
-  constexpr int EPI_BYTES = MODE == EPI_QKV ? qkv_epi_bytes<WBM, WBN, NT>() : 0;
+  constexpr int WNW = 8 / WMW, MT = WBM / 32 / WMW, NT = BN / 32 / WNW;
+  static_assert(MT * 32 * WMW == WBM && NT * 32 * WNW == BN && BN % 64 == 0, "wide tile shape");
+  constexpr int STAGE = (WBM + BN) * WBK;  // bf16 elements per stage
+  constexpr int MAIN_BYTES = 2 * STAGE * 2;
+  constexpr int EPI_BYTES = MODE == EPI_QKV ? qkv_epi_bytes<WBM, BN, NT>() : 0;
   constexpr int LDS_BYTES = MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES;
   __shared__ __attribute__((aligned(1024))) char lds[LDS_BYTES];
   bf16* sbuf = reinterpret_cast<bf16*>(lds);
 
-  const int n_tm = (M + WBM - 1) / WBM, n_tn = N / WBN;
+  const int n_tm = (M + WBM - 1) / WBM, n_tn = N / BN;
   const int total = n_tm * n_tn;
   const int per_xcd = (total + kXcd - 1) / kXcd;
   const int t = (blockIdx.x % kXcd) * per_xcd + blockIdx.x / kXcd;
@@ -582,17 +585,17 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_wide(const bf16* __restrict_
   const int first_m = (t / in_group) * GM;
   const int gm = min(GM, n_tm - first_m);
   const int tm = first_m + (t % in_group) % gm, tn = (t % in_group) / gm;
-  const int m0 = tm * WBM, n0 = tn * WBN;
+  const int m0 = tm * WBM, n0 = tn * BN;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 2, wn = wave & 3;
+  const int wm = wave / WNW, wn = wave % WNW;
   const int hi = lane >> 5, lo = lane & 31;
   const bf16* Ab = A + (long long)m0 * K;
   const bf16* Wb = W + (long long)n0 * K;
-  // DMA request I (0..31) of an operand fills its rows 8I .. 8I+7 lane-
-  // linearly (lane l: row 8I + l/8, physical chunk l%8, which holds the
-  // logical chunk swz8(row, l%8)); wave w issues I = w + 8i, i = 0..3
+  // DMA request I of an operand (A: 0..31, W: 0..BN/8-1) fills its rows
+  // 8I .. 8I+7 lane-linearly (lane l: row 8I + l/8, physical chunk l%8, which
+  // holds the logical chunk swz8(row, l%8)); wave w issues I = w + 8i
   int goff[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -614,16 +617,16 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_wide(const bf16* __restrict_
 
   const int KT = K / WBK;
   auto issue = [&](int kt, int buf) __attribute__((always_inline)) {
-    bf16* sa = sbuf + buf * WSTAGE;
+    bf16* sa = sbuf + buf * STAGE;
     bf16* sb = sa + WBM * WBK;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) dma16(Ab + goff[i] + kt * WBK, sa + (wave + 8 * i) * 512);
+    for (int i = 0; i < WBM / 64; ++i) dma16(Ab + goff[i] + kt * WBK, sa + (wave + 8 * i) * 512);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) dma16(Wb + goff[i] + kt * WBK, sb + (wave + 8 * i) * 512);
+    for (int i = 0; i < BN / 64; ++i) dma16(Wb + goff[i] + kt * WBK, sb + (wave + 8 * i) * 512);
   };
   auto compute = [&](int buf) __attribute__((always_inline)) {
-    const bf16* sa = sbuf + buf * WSTAGE + (wm * MT * 32) * WBK;
-    const bf16* sb = sbuf + buf * WSTAGE + WBM * WBK + (wn * NT * 32) * WBK;
+    const bf16* sa = sbuf + buf * STAGE + (wm * MT * 32) * WBK;
+    const bf16* sb = sbuf + buf * STAGE + WBM * WBK + (wn * NT * 32) * WBK;
 #pragma unroll
     for (int kk = 0; kk < WBK / 16; ++kk) {
       bf16x8 a[MT], b[NT];
@@ -661,7 +664,7 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_wide(const bf16* __restrict_
 #undef XC_WAIT_VMCNT0
 
   if constexpr (MODE == EPI_QKV) {
-    qkv_epilogue<MT, NT, WBM, WBN, 512>(e, acc, lds, m0, n0, M, wm, wn, tid, hi, lo);
+    qkv_epilogue<MT, NT, WBM, BN, 512>(e, acc, lds, m0, n0, M, wm, wn, tid, hi, lo);
   } else {
     tile_epilogue<MODE, MT, NT>(e, acc, m0, wm * MT * 32 + hi * 4, n0 + wn * NT * 32 + lo, M, WBM);
   }
@@ -999,24 +1002,27 @@ void launch_bf16(const void* A, const void* W, int M, int N, int K, const EpiArg
   gemm_bf16_kernel<MODE, MT, 2><<<grid, 256, 0, st>>>((const bf16*)A, (const bf16*)W, M, N, K, e, flag);
 }
 
-template <int MODE>
+template <int MODE, int BN, int WMW>
 void launch_wide(const void* A, const void* W, int M, int N, int K, const EpiArgs& e, const int* flag,
                  hipStream_t st) {
-  const int tiles = ((M + WBM - 1) / WBM) * (N / WBN);
+  const int tiles = ((M + WBM - 1) / WBM) * (N / BN);
   const int grid = (tiles + kXcd - 1) / kXcd * kXcd;
-  gemm_bf16_wide<MODE><<<grid, 512, 0, st>>>((const bf16*)A, (const bf16*)W, M, N, K, e, flag);
+  gemm_bf16_wide<MODE, BN, WMW><<<grid, 512, 0, st>>>((const bf16*)A, (const bf16*)W, M, N, K, e, flag);
 }
 
 template <int MODE>
 void launch_mode(int dtype, const void* A, const void* W, int M, int N, int K, const EpiArgs& e, const int* flag,
                  hipStream_t st) {
   if (dtype == 1) {
-    // the QKV and MLP-up products on the wide kernel (measured at the
-    // multi-camera shapes: 115 us against 140 us for QKV, 156 us against
-    // 190 us for MLP-up, on the two-workgroup kernel)
+    // the QKV and MLP-up products on 256 x 256 wide tiles (measured at the
+    // multi-camera shapes against the two-workgroup kernel: QKV 115 vs
+    // 140 us, MLP-up 156 vs 190 us).  The output and MLP-down projections stay
+    // on the persistent kernel: 256 x 192 wide tiles measured 52 vs 49 us
+    // for the output projection and, in the full pass (with the column-sum
+    // epilogue), 151 vs 145 us for MLP-down.
     if constexpr (MODE == EPI_QKV || MODE == EPI_UP) {
-      if (N % WBN == 0 && K % WBK == 0 && (MODE != EPI_QKV || (e.H * e.D) % WBN == 0)) {
-        launch_wide<MODE>(A, W, M, N, K, e, flag, st);
+      if (N % 256 == 0 && K % WBK == 0 && (MODE != EPI_QKV || (e.H * e.D) % 256 == 0)) {
+        launch_wide<MODE, 256, 2>(A, W, M, N, K, e, flag, st);
         return;
       }
     }
