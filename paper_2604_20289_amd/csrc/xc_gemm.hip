@@ -541,8 +541,10 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(const bf16* __restric
 // requests, as in the 32-deep stages above, measured at 14 TB/s of global ->
 // LDS throughput against 22 TB/s for 128-byte ones), and per output element a
 // 256 x 256 tile moves a third fewer operand bytes than two 256 x 128 tiles.
-// Two 64 KB stages fit in LDS: the next stage is requested at the top of a
-// step, while the current one is multiplied.  LDS rows are 128 bytes with
+// The weights have a ring of three 32 KB stage slots and the activations one
+// of two (160 KB for 256 x 256 tiles): weights are requested two steps ahead,
+// activations one step ahead, both at the top of a step while the current
+// stage is multiplied.  LDS rows are 128 bytes with
 // their 16-byte chunks XOR-swizzled (swz8) so the 32 rows a half-wave reads
 // at one chunk position fall in distinct banks.  256 x 256 tiles serve the
 // QKV and MLP-up projections (N % 256 == 0, K % 64 == 0, and C % 256 == 0 for
@@ -568,8 +570,8 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_wide(const bf16* __restrict_
   if (flag != nullptr && *flag) return;
   constexpr int WNW = 8 / WMW, MT = WBM / 32 / WMW, NT = BN / 32 / WNW;
   static_assert(MT * 32 * WMW == WBM && NT * 32 * WNW == BN && BN % 64 == 0, "wide tile shape");
-  constexpr int STAGE = (WBM + BN) * WBK;  // bf16 elements per stage
-  constexpr int MAIN_BYTES = 2 * STAGE * 2;
+  constexpr int ASLOT = WBM * WBK, WSLOT = BN * WBK;  // bf16 elements of one A / W stage slot
+  constexpr int MAIN_BYTES = (2 * ASLOT + 3 * WSLOT) * 2;  // A ring of 2, W ring of 3
   constexpr int EPI_BYTES = MODE == EPI_QKV ? qkv_epi_bytes<WBM, BN, NT>() : 0;
   constexpr int LDS_BYTES = MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES;
   __shared__ __attribute__((aligned(1024))) char lds[LDS_BYTES];
@@ -616,17 +618,19 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_wide(const bf16* __restrict_
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const int KT = K / WBK;
-  auto issue = [&](int kt, int buf) __attribute__((always_inline)) {
-    bf16* sa = sbuf + buf * STAGE;
-    bf16* sb = sa + WBM * WBK;
+  auto issue_a = [&](int kt, int slot) __attribute__((always_inline)) {
+    bf16* sa = sbuf + slot * ASLOT;
 #pragma unroll
     for (int i = 0; i < WBM / 64; ++i) dma16(Ab + goff[i] + kt * WBK, sa + (wave + 8 * i) * 512);
+  };
+  auto issue_w = [&](int kt, int slot) __attribute__((always_inline)) {
+    bf16* sb = sbuf + 2 * ASLOT + slot * WSLOT;
 #pragma unroll
     for (int i = 0; i < BN / 64; ++i) dma16(Wb + goff[i] + kt * WBK, sb + (wave + 8 * i) * 512);
   };
-  auto compute = [&](int buf) __attribute__((always_inline)) {
-    const bf16* sa = sbuf + buf * STAGE + (wm * MT * 32) * WBK;
-    const bf16* sb = sbuf + buf * STAGE + WBM * WBK + (wn * NT * 32) * WBK;
+  auto compute = [&](int aslot, int wslot) __attribute__((always_inline)) {
+    const bf16* sa = sbuf + aslot * ASLOT + (wm * MT * 32) * WBK;
+    const bf16* sb = sbuf + 2 * ASLOT + wslot * WSLOT + (wn * NT * 32) * WBK;
 #pragma unroll
     for (int kk = 0; kk < WBK / 16; ++kk) {
       bf16x8 a[MT], b[NT];
@@ -641,27 +645,41 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_wide(const bf16* __restrict_
           acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mt], b[nt], acc[mt][nt], 0, 0, 0);
     }
   };
-  // vmcnt(0) with the other counters left at their maximum (gfx9 encoding)
-#define XC_WAIT_VMCNT0() __builtin_amdgcn_s_waitcnt(0x3f70)
-  // stage k lives in buffer k mod 2; stage k+1 is requested at the top of
-  // step k (its buffer was released by the barrier that ended step k-1) and
-  // waited for at the bottom
-  issue(0, 0);
-  XC_WAIT_VMCNT0();
+  // A(k) lives in A slot k mod 2, W(k) in W slot k mod 3: the weights, which
+  // stream from HBM (the activations were just written and sit in the
+  // caches), are requested two steps ahead.  Step k requests A(k+1) and then
+  // W(k+2) (their slots were released by the barrier that ended step k-1),
+  // multiplies stage k, and waits for everything but the W(k+2) requests
+  // (vmcnt counts in issue order).
+#define XC_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt((0x3f70) | ((n) & 15) | (((n) >> 4) << 14))
+  constexpr int WREQ = BN / 64;
+  issue_w(0, 0);
+  issue_a(0, 0);
+  if (KT > 1) {
+    issue_w(1, 1);
+    XC_WAIT_VMCNT(WREQ);
+  } else {
+    XC_WAIT_VMCNT(0);
+  }
   __syncthreads();
-  auto step = [&](int kt, int b0) __attribute__((always_inline)) {
-    if (kt + 1 < KT) issue(kt + 1, b0 ^ 1);
-    compute(b0);
-    XC_WAIT_VMCNT0();
+  auto step = [&](int kt, int as, int ws) __attribute__((always_inline)) {
+    if (kt + 1 < KT) issue_a(kt + 1, as ^ 1);
+    if (kt + 2 < KT) issue_w(kt + 2, ws == 0 ? 2 : ws - 1);
+    compute(as, ws);
+    if (kt + 2 < KT) XC_WAIT_VMCNT(WREQ); else XC_WAIT_VMCNT(0);
     __syncthreads();
   };
   int kt = 0;
-  for (; kt + 1 < KT; kt += 2) {
-    step(kt, 0);
-    step(kt + 1, 1);
+  for (; kt + 5 < KT; kt += 6) {
+    step(kt, 0, 0);
+    step(kt + 1, 1, 1);
+    step(kt + 2, 0, 2);
+    step(kt + 3, 1, 0);
+    step(kt + 4, 0, 1);
+    step(kt + 5, 1, 2);
   }
-  if (kt < KT) step(kt, 0);
-#undef XC_WAIT_VMCNT0
+  for (; kt < KT; ++kt) step(kt, kt & 1, kt % 3);
+#undef XC_WAIT_VMCNT
 
   if constexpr (MODE == EPI_QKV) {
     qkv_epilogue<MT, NT, WBM, BN, 512>(e, acc, lds, m0, n0, M, wm, wn, tid, hi, lo);
