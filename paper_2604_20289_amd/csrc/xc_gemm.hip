@@ -250,173 +250,170 @@ __device__ __forceinline__ void qkv_epilogue(const EpiArgs& e, f32x16 (&acc)[MT]
                                              int M, int wm, int wn, int tid, int hi, int lo) {
   constexpr int NSLOT = BN / NT;  // column slots: (waves across N) x 32 lanes
   constexpr int SS = NSLOT + 5;   // row stride of the sums: the slots, up to 4 head scales, odd
-  {
-    const int C = e.H * e.D;
-    const int lpart = n0 / C;            // a tile never straddles two column blocks
-    const int part = lpart + e.part_base;  // 0 q, 1 k, 2 v
-    const int head0 = (n0 - lpart * C) / e.D;
+  const int C = e.H * e.D;
+  const int lpart = n0 / C;            // a tile never straddles two column blocks
+  const int part = lpart + e.part_base;  // 0 q, 1 k, 2 v
+  const int head0 = (n0 - lpart * C) / e.D;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const float bv = e.bias[n0 + wn * NT * 32 + nt * 32 + lo];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[mt][nt][r] += bv;
+    }
+  if (part < 2) {
+    // per (row, head) RMS over the head's D columns: lane partials -> LDS
+    float* ss = reinterpret_cast<float*>(lds);  // [BM][SS]
+    const int slot = wn * 32 + lo;             // NSLOT column slots of NT columns' squares each
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const float bv = e.bias[n0 + wn * NT * 32 + nt * 32 + lo];
+      for (int g = 0; g < 4; ++g)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[mt][nt][r] += bv;
-      }
-    if (part < 2) {
-      // per (row, head) RMS over the head's D columns: lane partials -> LDS
-      float* ss = reinterpret_cast<float*>(lds);  // [BM][SS]
-      const int slot = wn * 32 + lo;             // NSLOT column slots of NT columns' squares each
+        for (int r = 0; r < 4; ++r) {
+          float p = 0.f;
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int g = 0; g < 4; ++g)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            float p = 0.f;
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) p += acc[mt][nt][g * 4 + r] * acc[mt][nt][g * 4 + r];
-            ss[(wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r) * SS + slot] = p;
-          }
-      __syncthreads();
-      // heads per tile: BN / D; slots per head NSLOT / heads (a wave's columns lie in one head)
-      const int hpt = BN / e.D, sph = NSLOT / hpt;
-      for (int idx = tid; idx < BM * hpt; idx += NTHR) {
-        const int row = idx / hpt, hd = idx - row * hpt;
-        float sum = 0.f;
-        for (int j = 0; j < sph; ++j) sum += ss[row * SS + hd * sph + j];
-        ss[row * SS + NSLOT + hd] = 1.0f / sqrtf(sum / (float)e.D + 1e-6f);  // slots NSLOT + hd hold the scales
-      }
-      __syncthreads();
-      const float* gain = part == 0 ? e.gq : e.gk;
-      const bool rope = e.rope.tab != nullptr;
-      // rotary embedding, per column of this lane: the table entry of its pair
-      // at axis position 0, the entry stride per position, the position's bit
-      // offset in the packed row coordinates
-      int rbase[NT], rstride[NT], rshift[NT];
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int tcol = wn * NT * 32 + nt * 32 + lo;
-        int pair = (tcol - (tcol / e.D) * e.D) >> 1, a = 0;
-        if (pair >= e.rope.np[0]) {
-          pair -= e.rope.np[0];
-          a = 1;
-          if (pair >= e.rope.np[1]) {
-            pair -= e.rope.np[1];
-            a = 2;
-          }
+          for (int nt = 0; nt < NT; ++nt) p += acc[mt][nt][g * 4 + r] * acc[mt][nt][g * 4 + r];
+          ss[(wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r) * SS + slot] = p;
         }
-        rbase[nt] = e.rope.off[a] + pair;
-        rstride[nt] = e.rope.np[a];
-        rshift[nt] = 10 * a;
-      }
-      // normalise (and rotate) in place first, store afterwards: no store sits
-      // between the table loads, whose waits would otherwise also wait for it
+    __syncthreads();
+    // heads per tile: BN / D; slots per head NSLOT / heads (a wave's columns lie in one head)
+    const int hpt = BN / e.D, sph = NSLOT / hpt;
+    for (int idx = tid; idx < BM * hpt; idx += NTHR) {
+      const int row = idx / hpt, hd = idx - row * hpt;
+      float sum = 0.f;
+      for (int j = 0; j < sph; ++j) sum += ss[row * SS + hd * sph + j];
+      ss[row * SS + NSLOT + hd] = 1.0f / sqrtf(sum / (float)e.D + 1e-6f);  // slots NSLOT + hd hold the scales
+    }
+    __syncthreads();
+    const float* gain = part == 0 ? e.gq : e.gk;
+    const bool rope = e.rope.tab != nullptr;
+    // rotary embedding, per column of this lane: the table entry of its pair
+    // at axis position 0, the entry stride per position, the position's bit
+    // offset in the packed row coordinates
+    int rbase[NT], rstride[NT], rshift[NT];
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          // the table entries of this group of 4 rows are loaded together (one wait, not one per value)
-          float2 cs[4][NT];
-          if (rope) {
-            int packed[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r)  // rows past M: clamped, never stored
-              packed[r] = e.rope.pos[min(m0 + wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r, M - 1)];
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-#pragma unroll
-              for (int nt = 0; nt < NT; ++nt)
-                cs[r][nt] = e.rope.tab[rbase[nt] + ((packed[r] >> rshift[nt]) & 1023) * rstride[nt]];
-          }
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int trow = wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r;
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) {
-              const int tcol = wn * NT * 32 + nt * 32 + lo;
-              const int hd = tcol / e.D, dd = tcol - hd * e.D;
-              float v = acc[mt][nt][g * 4 + r] * ss[trow * SS + NSLOT + hd] * gain[dd];
-              if (rope) {
-                // rotary pair (dd & ~1, dd | 1) = lanes (lo & ~1, lo | 1) of the same row, swapped
-                // by a DPP quad permutation [1, 0, 3, 2]: (a, b) -> (a c - b s, a s + b c)
-                const float pv = __builtin_bit_cast(
-                    float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
-                v = v * cs[r][nt].x + ((lo & 1) ? pv : -pv) * cs[r][nt].y;
-              }
-              acc[mt][nt][g * 4 + r] = v;
-            }
-          }
+    for (int nt = 0; nt < NT; ++nt) {
+      const int tcol = wn * NT * 32 + nt * 32 + lo;
+      int pair = (tcol - (tcol / e.D) * e.D) >> 1, a = 0;
+      if (pair >= e.rope.np[0]) {
+        pair -= e.rope.np[0];
+        a = 1;
+        if (pair >= e.rope.np[1]) {
+          pair -= e.rope.np[1];
+          a = 2;
         }
-      // Stores: a wave's 32*NT columns lie in one head (NT*32 <= D), whose rows
-      // [m0, min(m0 + BM, M)) form one buffer range; the even lane of each
-      // column pair stores both values as one dword (the odd lane's offset is
-      // the range's end, so its store is dropped), and rows past M are dropped
-      // by the range check, so no branch separates the stores.
-      static_assert(NT * 32 <= 64, "one head per wave");
-      const int hd = (wn * NT * 32) / e.D;
-      const long long hh = head0 + hd;
-      const int rows = min(BM, M - m0);
-      bf16* hbase = part == 0 ? reinterpret_cast<bf16*>(e.q_out) + (hh * e.Mpad + m0) * e.D
-                              : reinterpret_cast<bf16*>(e.k_cache) + (hh * e.Lcap + e.kv_off + m0) * e.D;
-      const __amdgpu_buffer_rsrc_t dst = __builtin_amdgcn_make_buffer_rsrc(hbase, (short)0, rows * e.D * 2, 0x00020000);
+      }
+      rbase[nt] = e.rope.off[a] + pair;
+      rstride[nt] = e.rope.np[a];
+      rshift[nt] = 10 * a;
+    }
+    // normalise (and rotate) in place first, store afterwards: no store sits
+    // between the table loads, whose waits would otherwise also wait for it
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int g = 0; g < 4; ++g)
+      for (int g = 0; g < 4; ++g) {
+        // the table entries of this group of 4 rows are loaded together (one wait, not one per value)
+        float2 cs[4][NT];
+        if (rope) {
+          int packed[4];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int trow = wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r;
+          for (int r = 0; r < 4; ++r)  // rows past M: clamped, never stored
+            packed[r] = e.rope.pos[min(m0 + wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r, M - 1)];
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt) {
-              const int dd = (wn * NT * 32 + nt * 32 + lo) - hd * e.D;
-              const float v = acc[mt][nt][g * 4 + r];
+          for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+              cs[r][nt] = e.rope.tab[rbase[nt] + ((packed[r] >> rshift[nt]) & 1023) * rstride[nt]];
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int trow = wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r;
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) {
+            const int tcol = wn * NT * 32 + nt * 32 + lo;
+            const int hd = tcol / e.D, dd = tcol - hd * e.D;
+            float v = acc[mt][nt][g * 4 + r] * ss[trow * SS + NSLOT + hd] * gain[dd];
+            if (rope) {
+              // rotary pair (dd & ~1, dd | 1) = lanes (lo & ~1, lo | 1) of the same row, swapped
+              // by a DPP quad permutation [1, 0, 3, 2]: (a, b) -> (a c - b s, a s + b c)
               const float pv = __builtin_bit_cast(
                   float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
-              const unsigned two = (unsigned)__builtin_bit_cast(unsigned short, (bf16)v) |
-                                   ((unsigned)__builtin_bit_cast(unsigned short, (bf16)pv) << 16);
-              const int off = (lo & 1) ? rows * e.D * 2 : (trow * e.D + dd) * 2;
-              __builtin_amdgcn_raw_buffer_store_b32(two, dst, off, 0, 0);
+              v = v * cs[r][nt].x + ((lo & 1) ? pv : -pv) * cs[r][nt].y;
             }
+            acc[mt][nt][g * 4 + r] = v;
           }
-    } else {
-      // V^T: transpose the tile through LDS, then write rows of consecutive tokens
-      bf16* vt = reinterpret_cast<bf16*>(lds);  // [BN][BM + 8]
-      constexpr int VS = BM + 8;
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-          for (int g = 0; g < 4; ++g)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-              vt[(wn * NT * 32 + nt * 32 + lo) * VS + wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r] =
-                  (bf16)acc[mt][nt][g * 4 + r];
-      __syncthreads();
-      const int rows = min(BM, M - m0);
-      for (int idx = tid; idx < BN * (BM / 2); idx += NTHR) {
-        const int col = idx / (BM / 2), rp = (idx - col * (BM / 2)) * 2;
-        if (rp >= rows) continue;
-        const int hd = col / e.D, dd = col - hd * e.D;
-        bf16* dst = reinterpret_cast<bf16*>(e.vt_cache) + ((long long)(head0 + hd) * e.D + dd) * e.Lcap + e.kv_off + m0 + rp;
-        if (rp + 1 < rows) {
-          typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-          bf16x2 two = {vt[col * VS + rp], vt[col * VS + rp + 1]};
-          if (((e.kv_off + m0 + rp) & 1) == 0) {
-            *reinterpret_cast<bf16x2*>(dst) = two;
-          } else {
-            dst[0] = two[0];
-            dst[1] = two[1];
-          }
-        } else {
-          dst[0] = vt[col * VS + rp];
         }
+      }
+    // Stores: a wave's 32*NT columns lie in one head (NT*32 <= D), whose rows
+    // [m0, min(m0 + BM, M)) form one buffer range; the even lane of each
+    // column pair stores both values as one dword (the odd lane's offset is
+    // the range's end, so its store is dropped), and rows past M are dropped
+    // by the range check, so no branch separates the stores.
+    static_assert(NT * 32 <= 64, "one head per wave");
+    const int hd = (wn * NT * 32) / e.D;
+    const long long hh = head0 + hd;
+    const int rows = min(BM, M - m0);
+    bf16* hbase = part == 0 ? reinterpret_cast<bf16*>(e.q_out) + (hh * e.Mpad + m0) * e.D
+                            : reinterpret_cast<bf16*>(e.k_cache) + (hh * e.Lcap + e.kv_off + m0) * e.D;
+    const __amdgpu_buffer_rsrc_t dst = __builtin_amdgcn_make_buffer_rsrc(hbase, (short)0, rows * e.D * 2, 0x00020000);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int trow = wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r;
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) {
+            const int dd = (wn * NT * 32 + nt * 32 + lo) - hd * e.D;
+            const float v = acc[mt][nt][g * 4 + r];
+            const float pv = __builtin_bit_cast(
+                float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
+            const unsigned two = (unsigned)__builtin_bit_cast(unsigned short, (bf16)v) |
+                                 ((unsigned)__builtin_bit_cast(unsigned short, (bf16)pv) << 16);
+            const int off = (lo & 1) ? rows * e.D * 2 : (trow * e.D + dd) * 2;
+            __builtin_amdgcn_raw_buffer_store_b32(two, dst, off, 0, 0);
+          }
+        }
+  } else {
+    // V^T: transpose the tile through LDS, then write rows of consecutive tokens
+    bf16* vt = reinterpret_cast<bf16*>(lds);  // [BN][BM + 8]
+    constexpr int VS = BM + 8;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            vt[(wn * NT * 32 + nt * 32 + lo) * VS + wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r] =
+                (bf16)acc[mt][nt][g * 4 + r];
+    __syncthreads();
+    const int rows = min(BM, M - m0);
+    for (int idx = tid; idx < BN * (BM / 2); idx += NTHR) {
+      const int col = idx / (BM / 2), rp = (idx - col * (BM / 2)) * 2;
+      if (rp >= rows) continue;
+      const int hd = col / e.D, dd = col - hd * e.D;
+      bf16* dst = reinterpret_cast<bf16*>(e.vt_cache) + ((long long)(head0 + hd) * e.D + dd) * e.Lcap + e.kv_off + m0 + rp;
+      if (rp + 1 < rows) {
+        typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+        bf16x2 two = {vt[col * VS + rp], vt[col * VS + rp + 1]};
+        if (((e.kv_off + m0 + rp) & 1) == 0) {
+          *reinterpret_cast<bf16x2*>(dst) = two;
+        } else {
+          dst[0] = two[0];
+          dst[1] = two[1];
+        }
+      } else {
+        dst[0] = vt[col * VS + rp];
       }
     }
   }
 }
-
 
 template <int MODE, int MT, int NT>
 __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(const bf16* __restrict__ A, const bf16* __restrict__ W,
