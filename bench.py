@@ -606,6 +606,11 @@ def main():
     if "roofline" in res and ceil32 > 0:
         res["mfma_ceiling"]["attention_frac_of_32x32x16"] = round(res["roofline"]["achieved"] / ceil32, 4)
     log(f"mfma ceiling: {ceil32:.0f} TFLOP/s (32x32x16), {ceil16:.0f} TFLOP/s (16x16x32), random operands")
+    # the global -> LDS request stream the GEMMs stage operands with, by the
+    # row segment one request fetches (why the wide GEMM uses 64-deep stages)
+    res["lds_dma_rate"] = {"unit": "TB/s", **{f"rows_{rb}B": round(xcp.xc_lds_dma_rate(rb, torch.cuda.current_stream().cuda_stream), 2)
+                                             for rb in (64, 128, 256)}}
+    log(f"global -> LDS stream: {res['lds_dma_rate']}")
     if not args.no_cpu_baseline:
         log("cpu baseline: one oracle block at full shape ...")
         res["cpu_baseline"] = cpu_baseline(w, weights, args.seed)

@@ -350,6 +350,21 @@ xc_status xc_kernel_times(xc_handle* h, int32_t kind, int64_t* launches, double*
  * Errors: XC_ERR_INVALID_ARG (NULL tflops, unknown shape), XC_ERR_HIP. */
 xc_status xc_mfma_rate(int32_t shape, int32_t random_operands, void* stream, double* tflops);
 
+/* Measurement aid, not a step of the method: the rate of the global -> LDS
+ * request stream (global_load_lds_dwordx4) that the GEMMs stage their
+ * operands with, as a function of the row segment one request fetches.
+ * 1008 workgroups (two per CU) each stream 24 KB stages of the rows of one
+ * of 28 shared row blocks (33 MB in all, as the M-tiles of a GEMM share
+ * their rows) through a 3-slot LDS ring two stages ahead, with no
+ * arithmetic; each stage takes row_bytes (64, 128 or 256) of every one of
+ * its 24 KB / row_bytes rows.  Allocates and frees the 33 MB source (zeros),
+ * runs on stream (a hipStream_t; NULL is the null stream), three untimed
+ * launches then the best of five timed ones, and waits for them;
+ * *tbytes_per_s receives TB/s moved into LDS.
+ * Errors: XC_ERR_INVALID_ARG (NULL output, other row_bytes), XC_ERR_OOM,
+ * XC_ERR_HIP. */
+xc_status xc_lds_dma_rate(int32_t row_bytes, void* stream, double* tbytes_per_s);
+
 #ifdef __cplusplus
 }
 #endif

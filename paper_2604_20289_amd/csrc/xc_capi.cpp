@@ -1337,6 +1337,14 @@ xc_status xc_mfma_rate(int32_t shape, int32_t random_operands, void* stream, dou
              : XC_ERR_HIP;
 }
 
+xc_status xc_lds_dma_rate(int32_t row_bytes, void* stream, double* tbytes_per_s) {
+  if (!tbytes_per_s || (row_bytes != 64 && row_bytes != 128 && row_bytes != 256)) return XC_ERR_INVALID_ARG;
+  *tbytes_per_s = 0.0;
+  const hipError_t e = lds_dma_rate(row_bytes, reinterpret_cast<hipStream_t>(stream), tbytes_per_s);
+  if (e == hipErrorOutOfMemory) return XC_ERR_OOM;
+  return e == hipSuccess ? XC_OK : XC_ERR_HIP;
+}
+
 xc_status xc_profile(xc_handle* h, int32_t enable) {
   if (!h) return XC_ERR_INVALID_ARG;
   h->profiling = enable != 0;

@@ -1,6 +1,8 @@
-// Measurement aid (not a step of the method): the bf16 MFMA rate the chip
+// Measurement aids (not steps of the method): the bf16 MFMA rate the chip
 // sustains on a loop that keeps every operand in registers, i.e. the
-// practical ceiling the contractions of the block can be compared with.
+// practical ceiling the contractions of the block can be compared with; and
+// the rate of the global -> LDS request stream the GEMMs stage their operands
+// with, as a function of the row segment one request fetches.
 //
 // Each wave repeats independent MFMA chains on operands it filled once: 4
 // chains of 32x32x16 or 16 chains of 16x16x32 (measured: with 4 waves per
@@ -78,7 +80,93 @@ __global__ __launch_bounds__(kDiagThreads) void mfma_loop_kernel(int iters, int 
   asm volatile("; mfma loop result %0" ::"v"(s));
 }
 
+// global -> LDS request stream: a workgroup streams tile t's rows (shared
+// with the other tiles of its row block, like the M-tiles of a GEMM) through
+// a 3-slot ring of 24 KB stages, two stages ahead, one barrier per stage and
+// no arithmetic; each stage takes RB bytes of every one of its 24 KB / RB
+// rows (RB = 64, 128 or 256: the row segment one request fetches).
+constexpr int kDmaGroups = 1008;
+constexpr int kDmaBlocks = 28;          // row blocks of 384 x 64-byte-stage rows shared by the tiles
+constexpr int kDmaRowElems = 1536;      // bf16 elements per matrix row
+
+__device__ __forceinline__ void dma16(const __bf16* src, __bf16* lds_block) {
+  __builtin_amdgcn_global_load_lds(src, lds_block, 16, 0, 0);
+}
+
+template <int RB>
+__global__ __launch_bounds__(256, 2) void dma_stream_kernel(const __bf16* __restrict__ A) {
+  __shared__ __attribute__((aligned(1024))) __bf16 lds[3][12 * 1024];
+  constexpr int CPR = RB / 16;                 // 16-byte chunks per row segment
+  constexpr int RPI = 64 / CPR;                // rows per 1 KB request
+  constexpr int ROWS = 24 * RPI;               // rows per stage
+  constexpr int STAGES = kDmaRowElems * 2 / RB;  // one pass over the rows
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const __bf16* base = A + (long long)(blockIdx.x % (kDmaBlocks * 384 / ROWS)) * ROWS * kDmaRowElems;
+  auto issue = [&](int st, int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < 6; ++i) {
+      const int I = wave + 4 * i;
+      const int row = I * RPI + lane / CPR, c = lane % CPR;
+      dma16(base + (long long)row * kDmaRowElems + st * (RB / 2) + c * 8, &lds[buf][I * 512]);
+    }
+  };
+#define XC_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt((0x3f70) | ((n) & 15) | (((n) >> 4) << 14))
+  issue(0, 0);
+  issue(1, 1);
+  XC_WAIT_VMCNT(6);
+  __syncthreads();
+  for (int st = 0; st < STAGES; ++st) {
+    issue(min(st + 2, STAGES - 1), (st + 2) % 3);
+    XC_WAIT_VMCNT(6);
+    __syncthreads();
+  }
+  XC_WAIT_VMCNT(0);
+#undef XC_WAIT_VMCNT
+}
+
 }  // namespace
+
+hipError_t lds_dma_rate(int row_bytes, hipStream_t st, double* tbps) {
+  const size_t elems = (size_t)kDmaBlocks * 384 * kDmaRowElems;
+  __bf16* A = nullptr;
+  hipError_t err = hipMalloc(&A, elems * sizeof(__bf16));
+  if (err != hipSuccess) return err;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  err = hipMemsetAsync(A, 0, elems * sizeof(__bf16), st);
+  if (err == hipSuccess) err = hipEventCreate(&e0);
+  if (err == hipSuccess) err = hipEventCreate(&e1);
+  auto launch = [&]() {
+    if (row_bytes == 64)
+      dma_stream_kernel<64><<<kDmaGroups, 256, 0, st>>>(A);
+    else if (row_bytes == 128)
+      dma_stream_kernel<128><<<kDmaGroups, 256, 0, st>>>(A);
+    else
+      dma_stream_kernel<256><<<kDmaGroups, 256, 0, st>>>(A);
+    return hipGetLastError();
+  };
+  float ms = 0.f;
+  for (int rep = 0; rep < 3 && err == hipSuccess; ++rep) err = launch();
+  for (int rep = 0; rep < 5 && err == hipSuccess; ++rep) {
+    float t = 0.f;
+    err = hipEventRecord(e0, st);
+    if (err == hipSuccess) err = launch();
+    if (err == hipSuccess) err = hipEventRecord(e1, st);
+    if (err == hipSuccess) err = hipEventSynchronize(e1);
+    if (err == hipSuccess) err = hipEventElapsedTime(&t, e0, e1);
+    if (err == hipSuccess && (ms == 0.f || t < ms)) ms = t;
+  }
+  if (e0 != nullptr) (void)hipEventDestroy(e0);
+  if (e1 != nullptr) (void)hipEventDestroy(e1);
+  const hipError_t ferr = hipStreamSynchronize(st);
+  (void)hipFree(A);
+  if (err != hipSuccess) return err;
+  if (ferr != hipSuccess) return ferr;
+  // every tile moves all 24 KB stages of one pass over its rows
+  const double bytes = (double)kDmaGroups * (kDmaRowElems * 2 / row_bytes) * 24.0 * 1024.0;
+  *tbps = ms > 0.f ? bytes / (ms * 1e-3) / 1e12 : 0.0;
+  return hipSuccess;
+}
 
 // Flops per wave and iteration: 4 x 32x32x16 products, or 16 x 16x16x32
 // products every second iteration: 131072 either way.  One untimed launch

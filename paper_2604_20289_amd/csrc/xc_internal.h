@@ -194,5 +194,8 @@ void launch_read_cache(int dtype, const void* src, float* out, int H, int R, int
 // Register-only MFMA loop (shape 0: 32x32x16, 1: 16x16x32 bf16), timed with
 // events on st; waits for it.
 hipError_t mfma_rate(int shape, int random, hipStream_t st, double* tflops);
+// global -> LDS stream of 24 KB stages with row_bytes (64 / 128 / 256) per
+// row and request; allocates and frees a 33 MB source; waits for it.
+hipError_t lds_dma_rate(int row_bytes, hipStream_t st, double* tbps);
 
 }  // namespace xc

@@ -37,7 +37,7 @@ KERNEL_NAMES = ["attention", "gemm_qkv", "gemm_oproj", "gemm_up", "gemm_down", "
 EXPORTED = ["xc_status_string", "xc_init", "xc_forward_chunk", "xc_forward_chunk_noalloc", "xc_kv_update",
             "xc_set_condition", "xc_read_cache", "xc_stats",
             "xc_reset", "xc_destroy", "xc_axpby", "xc_fingerprint_rows", "xc_profile", "xc_kernel_times",
-            "xc_mfma_rate"]
+            "xc_mfma_rate", "xc_lds_dma_rate"]
 
 
 class ViewGroupC(ctypes.Structure):
@@ -107,6 +107,7 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
         "xc_profile": (i32, [vp, i32]),
         "xc_kernel_times": (i32, [vp, i32, P(ctypes.c_int64), P(ctypes.c_double), i32]),
         "xc_mfma_rate": (i32, [i32, i32, vp, P(ctypes.c_double)]),
+        "xc_lds_dma_rate": (i32, [i32, vp, P(ctypes.c_double)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -263,6 +264,13 @@ def xc_mfma_rate(shape: int, random_operands: bool, stream: Optional[int] = None
     t = ctypes.c_double()
     _check(load_library().xc_mfma_rate(shape, 1 if random_operands else 0, stream or None, ctypes.byref(t)),
            "xc_mfma_rate")
+    return t.value
+
+
+def xc_lds_dma_rate(row_bytes: int, stream: Optional[int] = None) -> float:
+    """TB/s of the global -> LDS request stream with row_bytes (64, 128, 256) per row and request."""
+    t = ctypes.c_double()
+    _check(load_library().xc_lds_dma_rate(row_bytes, stream or None, ctypes.byref(t)), "xc_lds_dma_rate")
     return t.value
 
 

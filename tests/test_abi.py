@@ -147,13 +147,15 @@ def test_calls_on_null_handle():
     assert lib.xc_read_cache(None, xcp.XC_CACHE_KEYS, 0, 0, 1, 1) == xcp.XC_ERR_INVALID_ARG
 
 
-def test_mfma_rate_rejects_bad_arguments():
+def test_measurement_aids_reject_bad_arguments():
     """Checked before any HIP call: runs without a GPU."""
     lib = xcp.load_library()
     t = ctypes.c_double(-1.0)
     assert lib.xc_mfma_rate(0, 1, None, None) == xcp.XC_ERR_INVALID_ARG
     assert lib.xc_mfma_rate(2, 1, None, ctypes.byref(t)) == xcp.XC_ERR_INVALID_ARG
     assert lib.xc_mfma_rate(-1, 0, None, ctypes.byref(t)) == xcp.XC_ERR_INVALID_ARG
+    assert lib.xc_lds_dma_rate(128, None, None) == xcp.XC_ERR_INVALID_ARG
+    assert lib.xc_lds_dma_rate(96, None, ctypes.byref(t)) == xcp.XC_ERR_INVALID_ARG
 
 
 def test_weight_blob_size_includes_cross_attention_tensors():
