@@ -6,14 +6,14 @@
 // accumulation.  Both operands are K-contiguous (activations row-major,
 // weights [out][in]), so a lane's MFMA operand is one 16-byte LDS read, and
 // stage tiles go from global memory straight into LDS (global_load_lds).
-//  * gemm_bf16_kernel: (64*MT) x 128 tiles, two workgroups per CU; used for
-//    the fused QKV projection, the MLP-up projection and for widths that are
-//    not multiples of 192.
-//  * gemm_bf16_persistent: 256 x 192 tiles, one persistent workgroup per CU
-//    streaming its tiles through a 4-deep LDS ring; used for the output and
-//    MLP-down projections.
+//  * gemm_bf16_wide: one 8-wave workgroup per CU, 256 x 256 tiles (QKV,
+//    MLP up) or 256 x 192 tiles (output and MLP-down projections), 64-deep
+//    stages;
+//  * gemm_bf16_kernel: (64*MT) x 128 tiles, two workgroups per CU, 32-deep
+//    stages; widths the wide tiles do not divide.
 // Both run the element-wise epilogues through tile_epilogue (software-
-// pipelined operand loads, range-checked buffer stores).
+// pipelined operand loads, range-checked buffer stores) and the QKV epilogue
+// through qkv_epilogue.
 //
 // fp32 path: a plain LDS-tiled FMA GEMM (64x64 tiles, 4x4 per thread) used
 // for float32 models.
@@ -91,7 +91,7 @@ __device__ __forceinline__ void tile_epilogue(const EpiArgs& e, const f32x16 (&a
                                               int M, int BM) {
   constexpr bool kRes = MODE == EPI_OPROJ || MODE == EPI_DOWN;
   constexpr bool kXin = MODE == EPI_DOWN;
-  // the tile's rows [m0, min(m0 + PBM, M)) of every output, as buffer ranges
+  // the tile's rows [m0, min(m0 + BM, M)) of every output, as buffer ranges
   const long long rows = min(BM, M - m0);
   const __amdgpu_buffer_rsrc_t out_f = tile_rsrc(e.out_f32 + (long long)m0 * e.N, rows * e.N * 4);
   const __amdgpu_buffer_rsrc_t out_b =
@@ -533,19 +533,20 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(const bf16* __restric
 // Wide bf16 MFMA GEMM: one workgroup of 8 waves per CU owns a 256 x BN tile,
 // its waves in a WMW x (8 / WMW) arrangement: 256 x 256 tiles as 2 x 4 waves
 // of 128 x 64 (4 x 2 accumulators each, as in gemm_bf16_kernel), 256 x 192
-// tiles as 4 x 2 waves of 64 x 96 (2 x 3).  Stages are 64 deep: every DMA request
-// fetches 128 contiguous bytes of a row (a whole cache line; 64-byte
-// requests, as in the 32-deep stages above, measured at 14 TB/s of global ->
-// LDS throughput against 22 TB/s for 128-byte ones), and per output element a
-// 256 x 256 tile moves a third fewer operand bytes than two 256 x 128 tiles.
-// The weights have a ring of three 32 KB stage slots and the activations one
-// of two (160 KB for 256 x 256 tiles): weights are requested two steps ahead,
-// activations one step ahead, both at the top of a step while the current
-// stage is multiplied.  LDS rows are 128 bytes with
-// their 16-byte chunks XOR-swizzled (swz8) so the 32 rows a half-wave reads
-// at one chunk position fall in distinct banks.  256 x 256 tiles serve the
-// QKV and MLP-up projections (N % 256 == 0, K % 64 == 0, and C % 256 == 0 for
-// QKV).
+// tiles as 4 x 2 waves of 64 x 96 (2 x 3).  Stages are 64 deep: every DMA
+// request fetches 128 contiguous bytes of a row (a whole cache line; the
+// request stream measures 14.6 TB/s with the 64-byte segments of 32-deep
+// stages against 24.5 TB/s with 128-byte ones, xc_lds_dma_rate), and per
+// output element a 256 x 256 tile moves a third fewer operand bytes than two
+// 256 x 128 tiles.  The weights have a ring of three stage slots and the
+// activations one of two (160 KB for 256 x 256 tiles, 136 KB for 256 x 192):
+// weights are requested two steps ahead, activations one step ahead, both at
+// the top of a step while the current stage is multiplied.  LDS rows are 128
+// bytes with their 16-byte chunks XOR-swizzled (swz8) so the 32 rows a
+// half-wave reads at one chunk position fall in distinct banks.  256 x 256
+// tiles serve the QKV and MLP-up projections (N % 256 == 0, K % 64 == 0, and
+// C % 256 == 0 for QKV), 256 x 192 tiles the output and MLP-down projections
+// (N % 192 == 0).
 // ---------------------------------------------------------------------------
 constexpr int WBM = 256, WBK = 64;
 
@@ -685,247 +686,6 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_wide(const bf16* __restrict_
   }
 }
 
-// ---------------------------------------------------------------------------
-// Persistent bf16 MFMA GEMM for the large products.  One workgroup of 4 waves
-// per CU (the grid never exceeds the CU count); a workgroup owns a 256 x BN
-// output tile (BN = 64*NT) per turn, its waves in a 2x2 arrangement of
-// 128 x (32*NT) sub-tiles held as 4 x NT accumulators (in AGPRs).  Per output
-// element this needs a third less operand traffic from L2 than two resident
-// 256 x 128 workgroups.  A workgroup walks its tiles as one continuous stream
-// of K=32 stages through a 4-deep LDS ring filled straight from global memory
-// (global_load_lds_dwordx4) three stages ahead, so the first stages of the next
-// tile load while the current tile finishes and runs its epilogue.  The MFMA
-// operands of the next 16-wide K slice are read from LDS while the current
-// slice's MFMAs issue.  Tiles are dealt to workgroups in the grouped order
-// (8 M-tiles x all N-tiles), each XCD taking a contiguous range per turn.
-// Used for the element-wise epilogues; K must be a multiple of 128.
-// ---------------------------------------------------------------------------
-constexpr int PBM = 256;
-constexpr int PNB = 4;
-
-template <int NT>
-struct PTile {
-  static constexpr int BN = 64 * NT;
-  static constexpr int STAGE = (PBM + BN) * GBK;                 // bf16 elements per stage
-  static constexpr int A_INSTR = PBM / 64, B_INSTR = BN / 64;   // load instructions per wave and stage
-  static constexpr int LOADS = A_INSTR + B_INSTR;
-};
-
-__device__ __forceinline__ void grouped_tile(int j, int n_tm, int n_tn, int& tm, int& tn) {
-  constexpr int GM = 8;
-  const int in_group = GM * n_tn;
-  const int first_m = (j / in_group) * GM;
-  const int gm = min(GM, n_tm - first_m);
-  tm = first_m + (j % in_group) % gm;
-  tn = (j % in_group) / gm;
-}
-
-// vmcnt(n) lgkmcnt(0) (gfx9 encoding, expcnt left at its maximum)
-#define XC_WAIT_VM_LGKM0(n) __builtin_amdgcn_s_waitcnt(0x0070 | ((n) & 15) | (((n) >> 4) << 14))
-
-template <int MODE, int NT>
-__global__ __launch_bounds__(256, 1) void gemm_bf16_persistent(const bf16* __restrict__ A,
-                                                               const bf16* __restrict__ W, int M, int N, int K,
-                                                               EpiArgs e, const int* __restrict__ flag) {
-  if (flag != nullptr && *flag) return;
-  typedef PTile<NT> T;
-  // One LDS array per ring slot (slot = stage mod 4, a constant at every use
-  // after unrolling): the compiler then tracks which slot each LDS-DMA request
-  // writes and does not hold reads of other slots behind it.
-  __shared__ __attribute__((aligned(16))) bf16 stg0[T::STAGE];
-  __shared__ __attribute__((aligned(16))) bf16 stg1[T::STAGE];
-  __shared__ __attribute__((aligned(16))) bf16 stg2[T::STAGE];
-  __shared__ __attribute__((aligned(16))) bf16 stg3[T::STAGE];
-  auto stage = [&](int b) __attribute__((always_inline)) -> bf16* {
-    return b == 0 ? stg0 : (b == 1 ? stg1 : (b == 2 ? stg2 : stg3));
-  };
-
-  const int n_tm = (M + PBM - 1) / PBM, n_tn = N / T::BN, n_tiles = n_tm * n_tn;
-  const int G = gridDim.x;
-  const int slot = (G % kXcd == 0) ? (blockIdx.x % kXcd) * (G / kXcd) + blockIdx.x / kXcd : blockIdx.x;
-  if (slot >= n_tiles) return;
-  const int n_my = (n_tiles - 1 - slot) / G + 1;
-  const int KT = K / GBK;
-  const int n_stages = n_my * KT;
-
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
-  const int hi = lane >> 5, lo = lane & 31;
-  // A load instruction i of this wave fills stage rows (wave + 4i)*16 .. +15,
-  // lane-linearly: the lane's 16 bytes land at row (lane/4), physical chunk
-  // lane%4, which holds logical chunk (lane%4) ^ ((row/4)%4).
-  const int lrow = lane >> 2, lchunk = (lane & 3) ^ ((lrow >> 2) & 3);
-  const int ld_off = lrow * K + lchunk * 8;  // + (wave + 4i) * 16 * K
-
-  // Loader state: the next stage to request (its tile and K step).  Past the
-  // last stage the requests repeat it (in bounds, into a buffer that is never
-  // read), so every step of the loop is the same code.
-  int ld_i = 0, ld_kt = 0;
-  const bf16* ldA;
-  const bf16* ldW;
-  auto ld_tile = [&](int i) __attribute__((always_inline)) {
-    int tm, tn;
-    grouped_tile(slot + i * G, n_tm, n_tn, tm, tn);
-    ldA = A + (long long)tm * PBM * K + ld_off;
-    ldW = W + (long long)tn * T::BN * K + ld_off;
-  };
-  ld_tile(0);
-  auto advance = [&]() __attribute__((always_inline)) {
-    if (ld_kt + 1 < KT) {
-      ++ld_kt;
-      ldA += GBK;
-      ldW += GBK;
-    } else if (ld_i + 1 < n_my) {
-      ld_kt = 0;
-      ld_tile(++ld_i);
-    }
-  };
-  auto issue = [&](int buf) __attribute__((always_inline)) {
-    bf16* sa = stage(buf);
-    bf16* sb = sa + PBM * GBK;
-#pragma unroll
-    for (int j = 0; j < T::A_INSTR; ++j)
-      __builtin_amdgcn_global_load_lds(ldA + (long long)(wave + 4 * j) * 16 * K, sa + (wave + 4 * j) * 512, 16, 0, 0);
-#pragma unroll
-    for (int j = 0; j < T::B_INSTR; ++j)
-      __builtin_amdgcn_global_load_lds(ldW + (long long)(wave + 4 * j) * 16 * K, sb + (wave + 4 * j) * 512, 16, 0, 0);
-    advance();
-  };
-  auto frags = [&](int buf, int kk, bf16x8* a, bf16x8* b) __attribute__((always_inline)) {
-    const bf16* sa = stage(buf);
-    const bf16* sb = sa + PBM * GBK;
-    const int c = kk * 2 + hi;
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt) a[mt] = *reinterpret_cast<const bf16x8*>(&sa[swz32(wm * 128 + mt * 32 + lo, c)]);
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-      b[nt] = *reinterpret_cast<const bf16x8*>(&sb[swz32(wn * NT * 32 + nt * 32 + lo, c)]);
-  };
-
-  auto mma = [&](f32x16 (&acc)[4][NT], const bf16x8* a, const bf16x8* b) __attribute__((always_inline)) {
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-        acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mt], b[nt], acc[mt][nt], 0, 0, 0);
-  };
-
-  // Stage q lives in LDS buffer q % 4.  At the barrier of step q every wave
-  // has read all of stage q (both K slices are in registers) and has seen its
-  // own loads of stage q+1 land; after it, stage q+4 is requested into
-  // stage q's buffer.  The inline barrier carries no memory fence, so the
-  // younger stages stay in flight across it.
-  bf16x8 a0[4], b0[NT], a1[4], b1[NT];
-  issue(0);
-  issue(1);
-  issue(2);
-  XC_WAIT_VM_LGKM0(2 * T::LOADS);
-  asm volatile("s_barrier" ::: "memory");
-  frags(0, 0, a0, b0);
-  // One step multiplies stage B (K slice 0 from a0/b0, slice 1 from a1/b1)
-  // and requests stage B+3 into the slot of stage B-1, which every wave left
-  // at the previous step's barrier.  A wave issues in order, so a DMA request
-  // that waits for the texture path holds back the MFMAs behind it: the 7
-  // requests are spread one at a time between the 3-MFMA groups of both
-  // slices (measured 5-7% faster than issuing them together), and the
-  // fragment reads of the next slice follow the first group.  The barrier
-  // sits between the slices; before it each wave waits for its own loads of
-  // stage B+1 (stage B+2 and the first 4 requests of B+3 may still fly) and
-  // for its slice-1 fragments.  The scheduling barriers pin the order.
-  static_assert(T::A_INSTR == 4 && T::B_INSTR == 3, "the request spread assumes 256 x 192 tiles");
-  auto grp = [&](f32x16 (&acc)[4][NT], const bf16x8* a, const bf16x8* b, int mt) __attribute__((always_inline)) {
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-      acc[mt][nt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mt], b[nt], acc[mt][nt], 0, 0, 0);
-    __builtin_amdgcn_sched_barrier(0);
-  };
-  // (the requests are written out one by one: wrapping the DMA builtin in a
-  // helper with a run-time choice between A and W keeps the compiler's host
-  // pass from emitting the kernel's launch stub)
-  auto step = [&](f32x16 (&acc)[4][NT], int B) __attribute__((always_inline)) {
-    bf16* sa = stage((B + 3) & 3);
-    bf16* sb = sa + PBM * GBK;
-    const bf16* gA = ldA;
-    const bf16* gW = ldW;
-    const long long r16 = 16LL * K;
-    __builtin_amdgcn_global_load_lds(gA + (wave + 0) * r16, sa + (wave + 0) * 512, 16, 0, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    grp(acc, a0, b0, 0);
-    __builtin_amdgcn_global_load_lds(gA + (wave + 4) * r16, sa + (wave + 4) * 512, 16, 0, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    frags(B, 1, a1, b1);
-    __builtin_amdgcn_sched_barrier(0);
-    grp(acc, a0, b0, 1);
-    __builtin_amdgcn_global_load_lds(gA + (wave + 8) * r16, sa + (wave + 8) * 512, 16, 0, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    grp(acc, a0, b0, 2);
-    __builtin_amdgcn_global_load_lds(gA + (wave + 12) * r16, sa + (wave + 12) * 512, 16, 0, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    grp(acc, a0, b0, 3);
-    XC_WAIT_VM_LGKM0(T::LOADS + T::A_INSTR);
-    asm volatile("s_barrier" ::: "memory");
-    __builtin_amdgcn_global_load_lds(gW + (wave + 0) * r16, sb + (wave + 0) * 512, 16, 0, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    grp(acc, a1, b1, 0);
-    __builtin_amdgcn_global_load_lds(gW + (wave + 4) * r16, sb + (wave + 4) * 512, 16, 0, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    frags((B + 1) & 3, 0, a0, b0);
-    __builtin_amdgcn_sched_barrier(0);
-    grp(acc, a1, b1, 1);
-    __builtin_amdgcn_global_load_lds(gW + (wave + 8) * r16, sb + (wave + 8) * 512, 16, 0, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    grp(acc, a1, b1, 2);
-    grp(acc, a1, b1, 3);
-    advance();
-    __builtin_amdgcn_sched_barrier(0);
-  };
-  // K is a multiple of 128, so every tile starts at slot 0
-  for (int ti = 0; ti < n_my; ++ti) {
-    f32x16 acc[4][NT];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < NT; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-    // Unrolled 16 steps deep where K allows: the compiler's own LDS-DMA
-    // bookkeeping drains all requests once per loop iteration.
-    int kt = 0;
-    for (; kt + 16 <= KT; kt += 16) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        step(acc, 0);
-        step(acc, 1);
-        step(acc, 2);
-        step(acc, 3);
-      }
-    }
-    for (; kt < KT; kt += 4) {
-      step(acc, 0);
-      step(acc, 1);
-      step(acc, 2);
-      step(acc, 3);
-    }
-    // ---- epilogue of local tile ti ----
-    int tm, tn;
-    grouped_tile(slot + ti * G, n_tm, n_tn, tm, tn);
-    const int m0 = tm * PBM, n0 = tn * T::BN;
-    // The per-lane row base is made opaque here so that the compiler derives
-    // the epilogue's addresses at the epilogue instead of keeping them live
-    // across the main loop.
-    int rb = wm * 128 + hi * 4;
-    asm volatile("" : "+v"(rb));
-    // accumulator element (mt, nt, g*4 + r): tile row wm*128 + mt*32 + g*8 + hi*4 + r,
-    // tile column wn*32*NT + nt*32 + lo
-    static_assert(MODE != EPI_QKV, "the fused QKV projection runs on the two-workgroup kernel");
-    tile_epilogue<MODE, 4, NT>(e, acc, m0, rb, n0 + wn * NT * 32 + lo, M, PBM);
-  }
-  // no LDS request may still be landing when the workgroup retires
-  XC_WAIT_VM_LGKM0(0);
-}
-#undef XC_WAIT_VM_LGKM0
-
 template <int MODE>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__ A, const float* __restrict__ W,
                                                        int M, int N, int K, EpiArgs e, const int* __restrict__ flag) {
@@ -997,18 +757,6 @@ int pick_mt(int M, int N) {
   return best;
 }
 
-// Whether the persistent kernel (256 x 192 tiles) takes an M x N x K product.
-bool use_persistent(int N, int K) { return N % PTile<3>::BN == 0 && K % 128 == 0; }
-
-template <int MODE, int NT>
-void launch_persistent(const void* A, const void* W, int M, int N, int K, const EpiArgs& e, const int* flag,
-                       hipStream_t st) {
-  const int tiles = ((M + PBM - 1) / PBM) * (N / PTile<NT>::BN);
-  int grid = tiles < cu_count() ? tiles : cu_count();
-  if (grid >= kXcd) grid = grid / kXcd * kXcd;
-  gemm_bf16_persistent<MODE, NT><<<grid, 256, 0, st>>>((const bf16*)A, (const bf16*)W, M, N, K, e, flag);
-}
-
 template <int MODE, int MT>
 void launch_bf16(const void* A, const void* W, int M, int N, int K, const EpiArgs& e, const int* flag, hipStream_t st) {
   typedef GemmTile<MT, 2> T;
@@ -1029,24 +777,21 @@ template <int MODE>
 void launch_mode(int dtype, const void* A, const void* W, int M, int N, int K, const EpiArgs& e, const int* flag,
                  hipStream_t st) {
   if (dtype == 1) {
-    // the QKV and MLP-up products on 256 x 256 wide tiles (measured at the
-    // multi-camera shapes against the two-workgroup kernel: QKV 115 vs
-    // 140 us, MLP-up 156 vs 190 us).  The output and MLP-down projections stay
-    // on the persistent kernel: 256 x 192 wide tiles measured 52 vs 49 us
-    // for the output projection and, in the full pass (with the column-sum
-    // epilogue), 151 vs 145 us for MLP-down.
+    // Wide tiles, measured at the multi-camera shapes: the QKV and MLP-up
+    // products on 256 x 256 (QKV 115 vs 140 us, MLP-up 156 vs 190 us against
+    // the two-workgroup kernel); the output and MLP-down projections on
+    // 256 x 192 (the same box in one call: 49.6 vs 51.3 us and 145.6 vs
+    // 147.6 us in the full pass against a persistent 4-wave kernel with
+    // 32-deep stages, which this replaced; 256 x 256 tiles leave 168 tiles
+    // for 256 CUs at hidden 1536).  Other widths: the two-workgroup kernel.
     if constexpr (MODE == EPI_QKV || MODE == EPI_UP) {
       if (N % 256 == 0 && K % WBK == 0 && (MODE != EPI_QKV || (e.H * e.D) % 256 == 0)) {
         launch_wide<MODE, 256, 2>(A, W, M, N, K, e, flag, st);
         return;
       }
-    }
-    // the MLP-up product runs faster on the two-workgroup kernel (measured at
-    // the multi-camera shape: 158-164 us against 175-177 us for 256 x 192
-    // persistent tiles, whose 896 tiles make 3.5 rounds on 256 CUs)
-    if constexpr (MODE != EPI_QKV && MODE != EPI_UP) {
-      if (use_persistent(N, K)) {
-        launch_persistent<MODE, 3>(A, W, M, N, K, e, flag, st);
+    } else {
+      if (N % 192 == 0 && K % WBK == 0) {
+        launch_wide<MODE, 192, 4>(A, W, M, N, K, e, flag, st);
         return;
       }
     }
