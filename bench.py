@@ -551,6 +551,17 @@ def main():
         "ema_cos_tb": [[None if not np.isfinite(v) else round(float(v), 5) for v in row]
                        for row in np.asarray(st["ema"]).reshape(S, B)],
     }
+    # How close the gate runs to its threshold: with the adaptive threshold on
+    # its floor, a (t, b) whose running cosine lies within a relative 1e-3 of
+    # the floor takes decisions of which either is correct (the parity band),
+    # so `skip_rate` and `value` depend on rounding there; the alt_tau_floor
+    # and gate_stress legs decide outside it.
+    ema = np.asarray(st["ema"], dtype=np.float64)
+    ema = ema[np.isfinite(ema)]
+    if ema.size and w.gate.adaptive:
+        floor = float(w.gate.tau_floor)
+        res["ema_near_floor"] = {"tau_floor": floor, "within_1e-3": int(np.sum(np.abs(ema - floor) <= 1e-3 * floor)),
+                                 "gated_tb": int(ema.size)}
     if alt:
         res["alt_tau_floor"] = alt
     if stress:
