@@ -616,6 +616,8 @@ def main():
                            "mfma_32x32x16": round(ceil32, 1), "mfma_16x16x32": round(ceil16, 1)}
     if "roofline" in res and ceil32 > 0:
         res["mfma_ceiling"]["attention_frac_of_32x32x16"] = round(res["roofline"]["achieved"] / ceil32, 4)
+    if "block_tflops_effective" in res and ceil32 > 0:
+        res["mfma_ceiling"]["block_effective_frac_of_32x32x16"] = round(res["block_tflops_effective"] / ceil32, 4)
     log(f"mfma ceiling: {ceil32:.0f} TFLOP/s (32x32x16), {ceil16:.0f} TFLOP/s (16x16x32), random operands")
     # the global -> LDS request stream the GEMMs stage operands with, by the
     # row segment one request fetches (why the wide GEMM uses 64-deep stages)
