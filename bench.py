@@ -52,18 +52,18 @@ PEAK_HBM_GBS = 8000.0
 
 # HBM-side bytes per full-window attention op (main dispatch + merge of the
 # key-split partials) from the rocprofv3 FETCH_SIZE and WRITE_SIZE passes,
-# scaled by a 512 MiB copy-kernel calibration; valid only for the kernel
-# source they were taken on (sha1 prefix of the file).
+# scaled by a 512 MiB copy-kernel calibration; valid only for the workload and
+# the kernel source they were taken on (sha1 prefix of the file).
 MEASURED_TRAFFIC = {
     "attention": {"source": "paper_2604_20289_amd/csrc/xc_attention.hip", "sha1": "c40848a0aa57cc2b",
-                  "bytes": (359.9 + 88.6) * 1e6},
+                  "workload": "multi-camera-bf16-dit-20blk-h1536-L7020", "bytes": (359.9 + 88.6) * 1e6},
 }
 
 
-def measured_traffic(kernel):
+def measured_traffic(kernel, workload):
     import hashlib
     rec = MEASURED_TRAFFIC.get(kernel)
-    if not rec:
+    if not rec or rec["workload"] != workload:
         return None
     with open(os.path.join(ROOT, rec["source"]), "rb") as f:
         if hashlib.sha1(f.read()).hexdigest()[:16] != rec["sha1"]:
@@ -589,7 +589,7 @@ def main():
             ach = af / (a["avg_us"] * 1e-6) / 1e12
             res["roofline"] = {"kernel": "attention", "bound": "mfma", "achieved": round(ach, 1),
                                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
-                               "traffic": measured_traffic("attention"), "flops_per_launch": af, "avg_launch_us": round(a["avg_us"], 1)}
+                               "traffic": measured_traffic("attention", w.name), "flops_per_launch": af, "avg_launch_us": round(a["avg_us"], 1)}
         gem = {"gemm_qkv": 6.0, "gemm_oproj": 2.0, "gemm_up": 2.0 * m.mlp_hidden / m.hidden,
                "gemm_down": 2.0 * m.mlp_hidden / m.hidden}
         res["kernels_full_compute"] = {}
