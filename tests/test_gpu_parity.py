@@ -3,6 +3,7 @@
 fp32 model: max-abs 1e-4 on every pass output.  bf16 models: relative L2
 2e-2.  Decisions must agree wherever a metric is outside a relative 1e-3 band
 around its threshold (see ``lockstep``)."""
+import dataclasses
 import math
 
 import numpy as np
@@ -450,5 +451,41 @@ def test_bf16_small_cameras_read_the_block_input():
     try:
         st = ls.run(5, tol_rel_l2=TOLBF)
         print(f"[parity] bf16-small-cameras skips={st['skips']} band={ls.band_hits}", flush=True)
+    finally:
+        ls.close()
+
+
+def _tiny(base, name, group, **stream):
+    w = synth.with_stream(synth.with_model(base, groups=(group,)), n_chunks=4, **stream)
+    return dataclasses.replace(w, name=name)
+
+
+TINY = {
+    "fp32-L1": _tiny(W0, "tiny-fp32-2blk-h128-L1", synth.ViewGroup(1, 1, 1, 1), rho=0.999),
+    "fp32-L33": _tiny(W0, "tiny-fp32-2blk-h128-L33", synth.ViewGroup(1, 1, 3, 11), rho=0.999),
+    "bf16-L1": _tiny(BF_RAGGED, "tiny-bf16-3blk-h256-L1", synth.ViewGroup(1, 1, 1, 1)),
+    "bf16-L33": _tiny(BF_RAGGED, "tiny-bf16-3blk-h256-L33", synth.ViewGroup(1, 1, 3, 11)),
+}
+
+
+@pytest.mark.parametrize("name", sorted(TINY))
+@pytest.mark.parametrize("gate", ["always-skip", "table1"])
+def test_tiny_token_counts(name, gate):
+    """Degenerate sizes: one token (every tile almost all padding, a camera of
+    one token whose fingerprint and mean are the token itself) and 33 tokens
+    (one past a 32-row block); both below the 64-key and 256-query tiles."""
+    w = TINY[name]
+    if gate == "always-skip":
+        w = synth.with_gate(w, adaptive=0, tau_cos_fixed=-1.0, tau_dev=math.inf)
+    else:
+        w = synth.with_gate(w, adaptive=1, tau_floor=0.97, tau_dev=2.0)
+    tol = dict(tol_abs=TOL32) if w.model.dtype == synth.F32 else dict(tol_rel_l2=TOLBF)
+    ls = _ls(w, compute=np.float32 if w.model.dtype == synth.BF16 else np.float64)
+    try:
+        st = ls.run(w.stream.n_chunks, **tol)
+        print(f"[parity] {name} {gate}: skips={st['skips']} of {st['evals_post_warmup']} band={ls.band_hits} "
+              f"worst={max(ls.worst.values()):.2e}", flush=True)
+        if gate == "always-skip":
+            assert st["skips"] > 0
     finally:
         ls.close()
