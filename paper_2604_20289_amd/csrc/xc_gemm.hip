@@ -28,6 +28,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 // tanh-approximated GELU, 0.5 v (1 + tanh(u)) with u = sqrt(2/pi) (v + 0.044715 v^3),
 // evaluated through the identity 0.5 (1 + tanh(u)) = 1 / (1 + e^(-2u)):
@@ -230,11 +231,60 @@ struct GemmTile {
 
 __device__ __forceinline__ int swz32(int row, int c) { return row * GBK + ((c ^ ((row >> 2) & 3)) << 3); }
 
-// LDS bytes of the QKV epilogue: row sums of squares [BM][BN/NT + 5] floats,
-// reused as the V^T transpose buffer [BN][BM + 8] bf16.
+// LDS bytes of the QKV epilogue: q / k stage the tile row-major [BM][BN + 8]
+// bf16 followed by two [waves across N][BM] float arrays (partial sums of
+// squares, scales); v transposes it through [BN][BM + 8] bf16.
 template <int BM, int BN, int NT>
 constexpr int qkv_epi_bytes() {
-  return BM * (BN / NT + 5) * 4 > BN * (BM + 8) * 2 ? BM * (BN / NT + 5) * 4 : BN * (BM + 8) * 2;
+  return BM * (BN + 8) * 2 + 2 * (BN / (NT * 32)) * BM * 4 > BN * (BM + 8) * 2
+             ? BM * (BN + 8) * 2 + 2 * (BN / (NT * 32)) * BM * 4
+             : BN * (BM + 8) * 2;
+}
+
+// two floats as bf16 (round to nearest even), the first in the low half
+__device__ __forceinline__ unsigned pack_bf16x2(float a, float b) {
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const f32x2 f = {a, b};
+  return __builtin_bit_cast(unsigned, __builtin_convertvector(f, bf16x2));
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+
+// One halving step of a reduce-scatter across a lane bit: partner lanes (the
+// DPP permutation CTRL pairs lanes that differ in that bit) swap halves of
+// their HALF-pairs; the lane with the bit set keeps the upper half.
+template <int CTRL, int HALF, int KP>
+__device__ __forceinline__ void rs_step(float (&v)[KP], bool upper) {
+#pragma unroll
+  for (int i = 0; i < HALF; ++i) {
+    const float send = upper ? v[i] : v[i + HALF], keep = upper ? v[i + HALF] : v[i];
+    v[i] = keep + dpp_move<CTRL>(send);
+  }
+}
+
+// Reduce-scatter of KP values per lane over the 32 lanes of each half-wave:
+// afterwards lane lo (0..31) holds in v[j], j < KP / 32, the half-wave sum of
+// value lo * KP / 32 + j.  Five halving steps, across lane bits 4 (the two
+// 16-lane rows, permlane16 swap: row 0 keeps the lower half), 3 (row mirror),
+// 2 (half-row mirror), 1 and 0 (quad permutations); 31 KP / 32 additions
+// instead of the 5 KP of a butterfly per value.
+template <int KP>
+__device__ __forceinline__ void half_wave_reduce_scatter(float (&v)[KP], int lo) {
+  static_assert(KP % 32 == 0, "whole values per lane");
+#pragma unroll
+  for (int i = 0; i < KP / 2; ++i) {
+    const auto pr =
+        __builtin_amdgcn_permlane16_swap(__float_as_uint(v[i]), __float_as_uint(v[i + KP / 2]), false, false);
+    v[i] = __uint_as_float(pr[0]) + __uint_as_float(pr[1]);
+  }
+  rs_step<0x140, KP / 4>(v, (lo & 8) != 0);
+  rs_step<0x141, KP / 8>(v, (lo & 4) != 0);
+  rs_step<0x4E, KP / 16>(v, (lo & 2) != 0);
+  rs_step<0xB1, KP / 32>(v, (lo & 1) != 0);
 }
 
 // QKV epilogue of a BM x BN tile (C = H*D columns per part, C % BN == 0, so a
@@ -244,60 +294,82 @@ constexpr int qkv_epi_bytes() {
 // waves hold MT x NT accumulators each at rows wm*MT*32.., columns
 // wn*NT*32..; NTHR threads; lds holds qkv_epi_bytes<BM, BN, NT>() bytes.
 // accumulator element (mt, nt, g, r): tile row wm*MT*32 + mt*32 + g*8 + hi*4 + r,
-// tile column wn*NT*32 + nt*32 + lo
+// tile column wn*NT*32 + nt*32 + lo.  A wave's NT*32 = 64 columns lie in one
+// head (D in {64, 128}).
 template <int MT, int NT, int BM, int BN, int NTHR>
-__device__ __forceinline__ void qkv_epilogue(const EpiArgs& e, f32x16 (&acc)[MT][NT], char* lds, int m0, int n0,
+__device__ __forceinline__ void qkv_epilogue(const EpiArgs& e, const f32x16 (&acc)[MT][NT], char* lds, int m0, int n0,
                                              int M, int wm, int wn, int tid, int hi, int lo) {
-  constexpr int NSLOT = BN / NT;  // column slots: (waves across N) x 32 lanes
-  constexpr int SS = NSLOT + 5;   // row stride of the sums: the slots, up to 4 head scales, odd
+  constexpr int WNW = BN / (NT * 32);  // waves across N
+  static_assert(NT * 32 == 64, "one head per wave");
   const int C = e.H * e.D;
   const int lpart = n0 / C;            // a tile never straddles two column blocks
   const int part = lpart + e.part_base;  // 0 q, 1 k, 2 v
   const int head0 = (n0 - lpart * C) / e.D;
+  // the accumulators plus bias as independent values (no 16-wide register
+  // tuple stays live across the branches below)
+  float x[MT][NT][16];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const float bv = e.bias[n0 + wn * NT * 32 + nt * 32 + lo];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[mt][nt][r] += bv;
+      for (int r = 0; r < 16; ++r) {
+        x[mt][nt][r] = acc[mt][nt][r] + bv;
+        asm volatile("" : "+v"(x[mt][nt][r]));
+      }
     }
   if (part < 2) {
-    // per (row, head) RMS over the head's D columns: lane partials -> LDS
-    float* ss = reinterpret_cast<float*>(lds);  // [BM][SS]
-    const int slot = wn * 32 + lo;             // NSLOT column slots of NT columns' squares each
+    const float* gain = part == 0 ? e.gq : e.gk;
+    const int hd = (wn * NT * 32) / e.D;  // the wave's head within the tile
+    float gv[NT];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+    for (int nt = 0; nt < NT; ++nt) gv[nt] = gain[wn * NT * 32 + nt * 32 + lo - hd * e.D];
+    // per (row, head) sum of squares over the head's D columns: the lane's
+    // NT columns, then the half-wave's 32 lanes (value k = (mt*4 + g)*4 + r is
+    // row wm*MT*32 + mt*32 + g*8 + hi*4 + r), then the D / 64 waves of the head
+    constexpr int KV = MT * 16, KP = (KV + 31) / 32 * 32, KL = KP / 32;
+    float p[KP];
 #pragma unroll
-      for (int g = 0; g < 4; ++g)
+    for (int k = 0; k < KP; ++k) {
+      float q = 0.f;
+      if (k < KV) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float p = 0.f;
+        for (int nt = 0; nt < NT; ++nt) q += x[k >> 4][nt][k & 15] * x[k >> 4][nt][k & 15];
+      }
+      p[k] = q;
+    }
+    half_wave_reduce_scatter(p, lo);
+    float* red = reinterpret_cast<float*>(lds + BM * (BN + 8) * 2);  // [WNW][BM] the waves' partial sums
+    float* scl = red + WNW * BM;                 // [WNW][BM] the scales each wave reads
+    const int rw = wm * MT * 32 + hi * 4;        // the half-wave's first row
 #pragma unroll
-          for (int nt = 0; nt < NT; ++nt) p += acc[mt][nt][g * 4 + r] * acc[mt][nt][g * 4 + r];
-          ss[(wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r) * SS + slot] = p;
-        }
-    __syncthreads();
-    // heads per tile: BN / D; slots per head NSLOT / heads (a wave's columns lie in one head)
-    const int hpt = BN / e.D, sph = NSLOT / hpt;
-    for (int idx = tid; idx < BM * hpt; idx += NTHR) {
-      const int row = idx / hpt, hd = idx - row * hpt;
-      float sum = 0.f;
-      for (int j = 0; j < sph; ++j) sum += ss[row * SS + hd * sph + j];
-      ss[row * SS + NSLOT + hd] = 1.0f / sqrtf(sum / (float)e.D + 1e-6f);  // slots NSLOT + hd hold the scales
+    for (int j = 0; j < KL; ++j) {
+      const int k = lo * KL + j;
+      if (k < KV) red[wn * BM + rw + (k >> 4) * 32 + ((k >> 2) & 3) * 8 + (k & 3)] = p[j];
     }
     __syncthreads();
-    const float* gain = part == 0 ? e.gq : e.gk;
-    const bool rope = e.rope.tab != nullptr;
+    const int wph = e.D / (NT * 32), w0 = wn / wph * wph;  // the head's waves
+#pragma unroll
+    for (int j = 0; j < KL; ++j) {
+      const int k = lo * KL + j;
+      if (k < KV) {
+        const int row = rw + (k >> 4) * 32 + ((k >> 2) & 3) * 8 + (k & 3);
+        float sum = 0.f;
+        for (int w = w0; w < w0 + wph; ++w) sum += red[w * BM + row];
+        scl[wn * BM + row] = 1.0f / sqrtf(sum / (float)e.D + 1e-6f);
+      }
+    }
+    __syncthreads();
     // rotary embedding, per column of this lane: the table entry of its pair
     // at axis position 0, the entry stride per position, the position's bit
     // offset in the packed row coordinates
+    const bool rope = e.rope.tab != nullptr;
     int rbase[NT], rstride[NT], rshift[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      const int tcol = wn * NT * 32 + nt * 32 + lo;
-      int pair = (tcol - (tcol / e.D) * e.D) >> 1, a = 0;
-      if (pair >= e.rope.np[0]) {
+      int pair = (wn * NT * 32 + nt * 32 + lo - hd * e.D) >> 1, a = 0;
+      if (rope && pair >= e.rope.np[0]) {
         pair -= e.rope.np[0];
         a = 1;
         if (pair >= e.rope.np[1]) {
@@ -305,111 +377,140 @@ __device__ __forceinline__ void qkv_epilogue(const EpiArgs& e, f32x16 (&acc)[MT]
           a = 2;
         }
       }
-      rbase[nt] = e.rope.off[a] + pair;
-      rstride[nt] = e.rope.np[a];
+      rbase[nt] = rope ? e.rope.off[a] + pair : 0;
+      rstride[nt] = rope ? e.rope.np[a] : 0;
       rshift[nt] = 10 * a;
     }
-    // normalise (and rotate) in place first, store afterwards: no store sits
-    // between the table loads, whose waits would otherwise also wait for it
+    // Normalise (and rotate) one group of 4 rows at a time and put it in
+    // LDS as bf16, row-major (the sums and scales sit behind the tile); the
+    // tile then leaves in 16-byte row chunks: tile row t of head h to
+    // q_out[h][m0 + t] or to token kv_off + m0 + t of the key cache.  The
+    // LDS offsets of a lane's values are compile-time immediates.
+    const float* sl4 = scl + wn * BM + rw;  // scales of the half-wave's rows
+    bf16* stg = reinterpret_cast<bf16*>(lds);
+    constexpr int SW = BN + 8;
+    bf16* sl = stg + rw * SW + wn * NT * 32 + lo;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        // the table entries of this group of 4 rows are loaded together (one wait, not one per value)
-        float2 cs[4][NT];
+        // scales of rows g*8 + hi*4 + 0..3 of 32-row block mt: one 16-byte read
+        const f32x4 sc = *reinterpret_cast<const f32x4*>(sl4 + mt * 32 + g * 8);
+        float y[4][NT];
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) y[r][nt] = x[mt][nt][g * 4 + r] * sc[r] * gv[nt];
         if (rope) {
+          // the group's table entries are loaded together (one wait, not one per value)
           int packed[4];
 #pragma unroll
           for (int r = 0; r < 4; ++r)  // rows past M: clamped, never stored
-            packed[r] = e.rope.pos[min(m0 + wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r, M - 1)];
+            packed[r] = e.rope.pos[min(m0 + rw + mt * 32 + g * 8 + r, M - 1)];
+          float2 cs[4][NT];
 #pragma unroll
           for (int r = 0; r < 4; ++r)
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt)
               cs[r][nt] = e.rope.tab[rbase[nt] + ((packed[r] >> rshift[nt]) & 1023) * rstride[nt]];
-        }
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int trow = wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r;
-#pragma unroll
-          for (int nt = 0; nt < NT; ++nt) {
-            const int tcol = wn * NT * 32 + nt * 32 + lo;
-            const int hd = tcol / e.D, dd = tcol - hd * e.D;
-            float v = acc[mt][nt][g * 4 + r] * ss[trow * SS + NSLOT + hd] * gain[dd];
-            if (rope) {
-              // rotary pair (dd & ~1, dd | 1) = lanes (lo & ~1, lo | 1) of the same row, swapped
-              // by a DPP quad permutation [1, 0, 3, 2]: (a, b) -> (a c - b s, a s + b c)
-              const float pv = __builtin_bit_cast(
-                  float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
-              v = v * cs[r][nt].x + ((lo & 1) ? pv : -pv) * cs[r][nt].y;
-            }
-            acc[mt][nt][g * 4 + r] = v;
-          }
-        }
-      }
-    // Stores: a wave's 32*NT columns lie in one head (NT*32 <= D), whose rows
-    // [m0, min(m0 + BM, M)) form one buffer range; the even lane of each
-    // column pair stores both values as one dword (the odd lane's offset is
-    // the range's end, so its store is dropped), and rows past M are dropped
-    // by the range check, so no branch separates the stores.
-    static_assert(NT * 32 <= 64, "one head per wave");
-    const int hd = (wn * NT * 32) / e.D;
-    const long long hh = head0 + hd;
-    const int rows = min(BM, M - m0);
-    bf16* hbase = part == 0 ? reinterpret_cast<bf16*>(e.q_out) + (hh * e.Mpad + m0) * e.D
-                            : reinterpret_cast<bf16*>(e.k_cache) + (hh * e.Lcap + e.kv_off + m0) * e.D;
-    const __amdgpu_buffer_rsrc_t dst = __builtin_amdgcn_make_buffer_rsrc(hbase, (short)0, rows * e.D * 2, 0x00020000);
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int g = 0; g < 4; ++g)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int trow = wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r;
-#pragma unroll
-          for (int nt = 0; nt < NT; ++nt) {
-            const int dd = (wn * NT * 32 + nt * 32 + lo) - hd * e.D;
-            const float v = acc[mt][nt][g * 4 + r];
-            const float pv = __builtin_bit_cast(
-                float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
-            const unsigned two = (unsigned)__builtin_bit_cast(unsigned short, (bf16)v) |
-                                 ((unsigned)__builtin_bit_cast(unsigned short, (bf16)pv) << 16);
-            const int off = (lo & 1) ? rows * e.D * 2 : (trow * e.D + dd) * 2;
-            __builtin_amdgcn_raw_buffer_store_b32(two, dst, off, 0, 0);
-          }
-        }
-  } else {
-    // V^T: transpose the tile through LDS, then write rows of consecutive tokens
-    bf16* vt = reinterpret_cast<bf16*>(lds);  // [BN][BM + 8]
-    constexpr int VS = BM + 8;
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-        for (int g = 0; g < 4; ++g)
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            vt[(wn * NT * 32 + nt * 32 + lo) * VS + wm * MT * 32 + mt * 32 + g * 8 + hi * 4 + r] =
-                (bf16)acc[mt][nt][g * 4 + r];
-    __syncthreads();
-    const int rows = min(BM, M - m0);
-    for (int idx = tid; idx < BN * (BM / 2); idx += NTHR) {
-      const int col = idx / (BM / 2), rp = (idx - col * (BM / 2)) * 2;
-      if (rp >= rows) continue;
-      const int hd = col / e.D, dd = col - hd * e.D;
-      bf16* dst = reinterpret_cast<bf16*>(e.vt_cache) + ((long long)(head0 + hd) * e.D + dd) * e.Lcap + e.kv_off + m0 + rp;
-      if (rp + 1 < rows) {
-        typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-        bf16x2 two = {vt[col * VS + rp], vt[col * VS + rp + 1]};
-        if (((e.kv_off + m0 + rp) & 1) == 0) {
-          *reinterpret_cast<bf16x2*>(dst) = two;
-        } else {
-          dst[0] = two[0];
-          dst[1] = two[1];
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+              // rotary pair (dd & ~1, dd | 1) = lanes (lo & ~1, lo | 1) of the same row, swapped
+              // by a DPP quad permutation [1, 0, 3, 2]: (a, b) -> (a c - b s, a s + b c)
+              const float pv = dpp_move<0xB1>(y[r][nt]);
+              y[r][nt] = y[r][nt] * cs[r][nt].x + ((lo & 1) ? pv : -pv) * cs[r][nt].y;
+            }
         }
-      } else {
-        dst[0] = vt[col * VS + rp];
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+          for (int r = 0; r < 4; r += 2) {
+            const unsigned w = pack_bf16x2(y[r][nt], y[r + 1][nt]);
+            sl[(mt * 32 + g * 8 + r) * SW + nt * 32] = __builtin_bit_cast(bf16, (unsigned short)w);
+            sl[(mt * 32 + g * 8 + r + 1) * SW + nt * 32] = __builtin_bit_cast(bf16, (unsigned short)(w >> 16));
+          }
+      }
+    __syncthreads();
+    constexpr int CPR = BN / 8, RPI = NTHR / CPR, ITER = BM / RPI;
+    static_assert(NTHR % CPR == 0 && BM % RPI == 0, "whole rows per pass");
+    const int cc = tid % CPR, row0 = tid / CPR;
+    const int hc = cc * 8 / e.D, dd = cc * 8 - hc * e.D;
+    const long long hh = head0 + hc;
+    const int rows = min(BM, M - m0);
+    bf16* dst = part == 0 ? reinterpret_cast<bf16*>(e.q_out) + (hh * e.Mpad + m0 + row0) * e.D + dd
+                          : reinterpret_cast<bf16*>(e.k_cache) + (hh * e.Lcap + e.kv_off + m0 + row0) * e.D + dd;
+    u32x4 ch[ITER];
+#pragma unroll
+    for (int it = 0; it < ITER; ++it) ch[it] = *reinterpret_cast<const u32x4*>(stg + (row0 + it * RPI) * SW + cc * 8);
+#pragma unroll
+    for (int it = 0; it < ITER; ++it)
+      if (row0 + it * RPI < rows) *reinterpret_cast<u32x4*>(dst + (long long)it * RPI * e.D) = ch[it];
+  } else {
+    // V^T: row head0*D + c of the cache holds column c of the tile, tokens
+    // contiguous.  The tile goes through LDS column-major, each column's
+    // token t at position s + t with s = (kv_off + m0) mod 8, so that 8-token
+    // chunks of a column (16 bytes at positions 8q..8q+7) start at a token
+    // index that is a multiple of 8 in the cache: 16-byte aligned stores.
+    // A lane holds tokens g*8 + hi*4 + 0..3 of its column: one 8-byte LDS
+    // write when s is a multiple of 4.
+    bf16* vt = reinterpret_cast<bf16*>(lds);  // [BN][VS]
+    constexpr int VS = BM + 8;
+    const int t0 = e.kv_off + m0;  // the tile's first token in the cache
+    const int s = t0 & 7;
+    bf16* vl = vt + (wn * NT * 32 + lo) * VS + s + wm * MT * 32 + hi * 4;
+    if ((s & 3) == 0) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+          for (int g = 0; g < 4; ++g)
+            *reinterpret_cast<uint2*>(vl + nt * 32 * VS + mt * 32 + g * 8) =
+                make_uint2(pack_bf16x2(x[mt][nt][g * 4], x[mt][nt][g * 4 + 1]),
+                           pack_bf16x2(x[mt][nt][g * 4 + 2], x[mt][nt][g * 4 + 3]));
+    } else {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+          for (int g = 0; g < 4; ++g)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) vl[nt * 32 * VS + mt * 32 + g * 8 + r] = (bf16)x[mt][nt][g * 4 + r];
+    }
+    __syncthreads();
+    // chunk q of column c: tile rows 8q - s .. 8q - s + 7, cache tokens
+    // t0 - s + 8q ..; rows outside [0, rows) are not stored
+    constexpr int QC = BM / 8 + 1, VIT = (BN * QC + NTHR - 1) / NTHR;
+    const int rows = min(BM, M - m0);
+    bf16* vbase = reinterpret_cast<bf16*>(e.vt_cache) + (long long)head0 * e.D * e.Lcap + (t0 - s);
+    const bool vec = ((reinterpret_cast<unsigned long long>(e.vt_cache) | ((unsigned long long)e.Lcap * 2)) & 15) == 0;
+    u32x4 ch[VIT];
+#pragma unroll
+    for (int it = 0; it < VIT; ++it) {
+      const int idx = tid + it * NTHR;
+      if (idx < BN * QC) {
+        const int c = idx / QC, q = idx - c * QC;
+        ch[it] = *reinterpret_cast<const u32x4*>(vt + c * VS + 8 * q);
+      }
+    }
+#pragma unroll
+    for (int it = 0; it < VIT; ++it) {
+      const int idx = tid + it * NTHR;
+      if (idx < BN * QC) {
+        const int c = idx / QC, q = idx - c * QC;
+        const int r0 = 8 * q - s;
+        bf16* dst = vbase + (long long)c * e.Lcap + 8 * q;
+        if (vec && r0 >= 0 && r0 + 8 <= rows) {
+          *reinterpret_cast<u32x4*>(dst) = ch[it];
+        } else {
+#pragma unroll
+          for (int i = 0; i < 8; ++i)
+            if (r0 + i >= 0 && r0 + i < rows)
+              dst[i] = __builtin_bit_cast(bf16, (unsigned short)(ch[it][i >> 1] >> (16 * (i & 1))));
+        }
       }
     }
   }
