@@ -614,11 +614,22 @@ def main():
     ceil16 = xcp.xc_mfma_rate(1, True, torch.cuda.current_stream().cuda_stream)
     res["mfma_ceiling"] = {"unit": "TFLOP/s", "operands": "random bf16",
                            "mfma_32x32x16": round(ceil32, 1), "mfma_16x16x32": round(ceil16, 1)}
+    # the same 32x32x16 loop at the attention kernel's occupancy under its
+    # instruction mix, on independent data: + one 16-byte LDS operand read per
+    # MFMA, + a 64-key softmax tile's VALU work per 32 MFMAs, both -- what the
+    # mix allows before any dependency or barrier is paid
+    mix = {name: xcp.xc_mfma_rate(shape, True, torch.cuda.current_stream().cuda_stream)
+           for name, shape in (("lds_reads", 2), ("softmax_valu", 3), ("lds_reads_and_softmax_valu", 4))}
+    res["mfma_ceiling"]["attention_mix_32x32x16"] = {k: round(v, 1) for k, v in mix.items()}
     if "roofline" in res and ceil32 > 0:
         res["mfma_ceiling"]["attention_frac_of_32x32x16"] = round(res["roofline"]["achieved"] / ceil32, 4)
+        if mix["lds_reads_and_softmax_valu"] > 0:
+            res["mfma_ceiling"]["attention_frac_of_its_mix"] = round(
+                res["roofline"]["achieved"] / mix["lds_reads_and_softmax_valu"], 4)
     if "block_tflops_effective" in res and ceil32 > 0:
         res["mfma_ceiling"]["block_effective_frac_of_32x32x16"] = round(res["block_tflops_effective"] / ceil32, 4)
-    log(f"mfma ceiling: {ceil32:.0f} TFLOP/s (32x32x16), {ceil16:.0f} TFLOP/s (16x16x32), random operands")
+    log(f"mfma ceiling: {ceil32:.0f} TFLOP/s (32x32x16), {ceil16:.0f} TFLOP/s (16x16x32), random operands; "
+        f"attention mix {res['mfma_ceiling']['attention_mix_32x32x16']}")
     # the global -> LDS request stream the GEMMs stage operands with, by the
     # row segment one request fetches (why the wide GEMM uses 64-deep stages)
     res["lds_dma_rate"] = {"unit": "TB/s", **{f"rows_{rb}B": round(xcp.xc_lds_dma_rate(rb, torch.cuda.current_stream().cuda_stream), 2)

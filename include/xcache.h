@@ -340,12 +340,18 @@ xc_status xc_kernel_times(xc_handle* h, int32_t kind, int64_t* launches, double*
 /* Measurement aid, not a step of the method: the bf16 MFMA rate the chip
  * sustains on a loop whose operands stay in registers (no memory traffic),
  * i.e. the practical ceiling of the contractions above.  shape: 0 =
- * v_mfma_f32_32x32x16_bf16, 1 = v_mfma_f32_16x16x32_bf16.  random_operands
- * != 0 fills the operands with random bf16 values of magnitude 0.5 to 2, 0
- * with zeros: the power the matrix cores draw, and with it the clock the
- * chip holds, depends on the operand bits.  Runs on stream (a hipStream_t;
- * NULL is the null stream) on the current device: one untimed launch, then
- * the best of three timed ones (about 40 ms in all); waits for them.
+ * v_mfma_f32_32x32x16_bf16, 1 = v_mfma_f32_16x16x32_bf16 (four waves per
+ * SIMD); 2-4 = 32x32x16 at the attention kernel's occupancy (one 512-thread
+ * workgroup per CU) under its instruction mix, on independent data: 2 = one
+ * 16-byte LDS operand read per MFMA, 3 = per 32 MFMAs the VALU work of one
+ * 64-key softmax tile (max of 32 scores, 32 fused scale-and-subtract, 32
+ * exp2, 16 bf16 pair conversions, 16 two-wide dot products), 4 = both.
+ * random_operands != 0 fills the operands with random bf16 values of
+ * magnitude 0.5 to 2, 0 with zeros: the power the matrix cores draw, and
+ * with it the clock the chip holds, depends on the operand bits.  Runs on
+ * stream (a hipStream_t; NULL is the null stream) on the current device: one
+ * untimed launch, then the best of three timed ones (about 40 ms in all for
+ * shapes 0 and 1, up to about 80 ms for the mixes); waits for them.
  * *tflops receives dense TFLOP/s (2 flops per multiply-add).
  * Errors: XC_ERR_INVALID_ARG (NULL tflops, unknown shape), XC_ERR_HIP. */
 xc_status xc_mfma_rate(int32_t shape, int32_t random_operands, void* stream, double* tflops);

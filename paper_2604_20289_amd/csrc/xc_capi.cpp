@@ -1330,7 +1330,7 @@ xc_status xc_fingerprint_rows(const xc_model_config* model, const xc_gate_config
 }
 
 xc_status xc_mfma_rate(int32_t shape, int32_t random_operands, void* stream, double* tflops) {
-  if (!tflops || (shape != 0 && shape != 1)) return XC_ERR_INVALID_ARG;
+  if (!tflops || shape < 0 || shape > 4) return XC_ERR_INVALID_ARG;
   *tflops = 0.0;
   return mfma_rate(shape, random_operands != 0, reinterpret_cast<hipStream_t>(stream), tflops) == hipSuccess
              ? XC_OK

@@ -2,7 +2,10 @@
 // sustains on a loop that keeps every operand in registers, i.e. the
 // practical ceiling the contractions of the block can be compared with; and
 // the rate of the global -> LDS request stream the GEMMs stage their operands
-// with, as a function of the row segment one request fetches.
+// with, as a function of the row segment one request fetches; and the MFMA
+// rate under the attention loop's instruction mix (its LDS operand reads and
+// its softmax VALU work) on data that depends on nothing, i.e. what that mix
+// allows before any dependency or synchronisation is paid.
 //
 // Each wave repeats independent MFMA chains on operands it filled once: 4
 // chains of 32x32x16 or 16 chains of 16x16x32 (measured: with 4 waves per
@@ -78,6 +81,72 @@ __global__ __launch_bounds__(kDiagThreads) void mfma_loop_kernel(int iters, int 
   }
   // the accumulators are consumed by an (empty) asm statement: the loop stays
   asm volatile("; mfma loop result %0" ::"v"(s));
+}
+
+// Instruction mixes of the attention loop at its occupancy (one 512-thread
+// workgroup per CU, two waves per SIMD; the 96 KB of LDS keep a second
+// workgroup off the CU).  Per wave and iteration: 32 MFMAs 32x32x16 on 4
+// chains with the B operand in registers and the A operand one of 8
+// fragment registers, which MIX bit 0 refills from LDS after each use (one
+// 16-byte read per MFMA, used 8 MFMAs later, from one of two 32 KB halves
+// by iteration: the attention kernel's K and V^T operand traffic); MIX bit 1 adds the VALU work a 64-key tile's softmax
+// costs a wave there: per lane the max of its 32 scores, 32 fused
+// scale-and-subtract, 32 exp2, 16 bf16 pair conversions and 16 two-wide dot
+// products for the row sum.  The probabilities become the next iteration's
+// scores, so nothing is loop-invariant and no extra instruction is needed.
+constexpr int kMixGroups = 256;
+constexpr int kMixThreads = 512;
+
+template <int MIX>
+__global__ __launch_bounds__(512, 1) void mfma_mix_kernel(int iters, int random, uint32_t seed) {
+  __shared__ __attribute__((aligned(1024))) __bf16 lds[48 * 1024];  // 96 KB; 64 fragment rows of 1 KB used
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  const int tid = threadIdx.x, lane = tid & 63;
+  uint32_t x = seed ^ ((blockIdx.x * kMixThreads + tid + 1u) * 0x9E3779B9u);
+  for (int i = tid; i < 64 * 512; i += kMixThreads) lds[i] = operand(x, random);
+  __syncthreads();
+  bf16x8 b, f[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) b[e] = operand(x, random);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) f[j] = *reinterpret_cast<const bf16x8*>(lds + j * 512 + lane * 8);
+  f32x16 acc[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[c][r] = 0.f;
+  float sc[32];
+#pragma unroll
+  for (int i = 0; i < 32; ++i) sc[i] = (float)((x >> (i & 15)) & 255) * (1.0f / 256.0f);
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  float m = 0.f, l = 0.f;
+  for (int it = 0; it < iters; ++it) {
+    const __bf16* half = lds + (it & 1) * 32 * 512 + lane * 8;  // the reads' offsets are immediates
+#pragma unroll
+    for (int j = 0; j < 32; ++j) {
+      acc[j & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[j & 7], b, acc[j & 3], 0, 0, 0);
+      if constexpr ((MIX & 1) != 0)
+        f[j & 7] = *reinterpret_cast<const bf16x8*>(half + j * 512);
+    }
+    if constexpr ((MIX & 2) != 0) {
+      float mx = m;
+#pragma unroll
+      for (int i = 0; i < 32; ++i) mx = fmaxf(mx, sc[i]);
+#pragma unroll
+      for (int i = 0; i < 32; ++i) sc[i] = __builtin_amdgcn_exp2f(fmaf(sc[i], 0.0884f, -mx));
+#pragma unroll
+      for (int i = 0; i < 32; i += 2) {
+        const f32x2 pf = {sc[i], sc[i + 1]};
+        l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_convertvector(pf, bf16x2), ones, l, false);
+      }
+      m = mx;
+    }
+  }
+  float t = l + m;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) t += acc[c][0];
+  asm volatile("; mfma mix result %0" ::"v"(t));
 }
 
 // global -> LDS request stream: a workgroup streams tile t's rows (shared
@@ -169,19 +238,23 @@ hipError_t lds_dma_rate(int row_bytes, hipStream_t st, double* tbps) {
 }
 
 // Flops per wave and iteration: 4 x 32x32x16 products, or 16 x 16x16x32
-// products every second iteration: 131072 either way.  One untimed launch
-// lets the clocks settle under the load; the best of three timed launches
-// (about 8 ms each) is reported.
+// products every second iteration: 131072 either way (shapes 0, 1); 32 x
+// 32x32x16 products = 1048576 for the mixes (shapes 2-4).  One untimed
+// launch lets the clocks settle under the load; the best of three timed
+// launches (about 8 ms each for shapes 0 and 1) is reported.
 hipError_t mfma_rate(int shape, int random, hipStream_t st, double* tflops) {
-  constexpr int kIters = 15000;
+  constexpr int kIters = 15000, kMixIters = 4000;
   hipEvent_t e0 = nullptr, e1 = nullptr;
   hipError_t err = hipEventCreate(&e0);
   if (err == hipSuccess) err = hipEventCreate(&e1);
   auto launch = [&](int iters) {
-    if (shape == 0)
-      mfma_loop_kernel<0><<<kDiagGroups, kDiagThreads, 0, st>>>(iters, random, 12345u);
-    else
-      mfma_loop_kernel<1><<<kDiagGroups, kDiagThreads, 0, st>>>(iters, random, 12345u);
+    switch (shape) {
+      case 0: mfma_loop_kernel<0><<<kDiagGroups, kDiagThreads, 0, st>>>(iters, random, 12345u); break;
+      case 1: mfma_loop_kernel<1><<<kDiagGroups, kDiagThreads, 0, st>>>(iters, random, 12345u); break;
+      case 2: mfma_mix_kernel<1><<<kMixGroups, kMixThreads, 0, st>>>(kMixIters, random, 12345u); break;
+      case 3: mfma_mix_kernel<2><<<kMixGroups, kMixThreads, 0, st>>>(kMixIters, random, 12345u); break;
+      default: mfma_mix_kernel<3><<<kMixGroups, kMixThreads, 0, st>>>(kMixIters, random, 12345u); break;
+    }
     return hipGetLastError();
   };
   float ms = 0.f;
@@ -198,7 +271,8 @@ hipError_t mfma_rate(int shape, int random, hipStream_t st, double* tflops) {
   if (e0 != nullptr) (void)hipEventDestroy(e0);
   if (e1 != nullptr) (void)hipEventDestroy(e1);
   if (err != hipSuccess) return err;
-  const double flops = (double)kDiagGroups * (kDiagThreads / 64) * kIters * 131072.0;
+  const double flops = shape < 2 ? (double)kDiagGroups * (kDiagThreads / 64) * kIters * 131072.0
+                                 : (double)kMixGroups * (kMixThreads / 64) * kMixIters * 1048576.0;
   *tflops = ms > 0.f ? flops / (ms * 1e-3) / 1e12 : 0.0;
   return hipSuccess;
 }

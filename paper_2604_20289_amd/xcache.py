@@ -260,7 +260,8 @@ def xc_kernel_times(h: int, kind: int, clear: bool = False):
 
 
 def xc_mfma_rate(shape: int, random_operands: bool, stream: Optional[int] = None) -> float:
-    """TFLOP/s of the register-only bf16 MFMA loop (shape 0: 32x32x16, 1: 16x16x32)."""
+    """TFLOP/s of the bf16 MFMA loop: shape 0 32x32x16, 1 16x16x32 (operands in registers); 2-4 the
+    attention loop's mix at its occupancy (2 + LDS operand reads, 3 + softmax VALU, 4 both)."""
     t = ctypes.c_double()
     _check(load_library().xc_mfma_rate(shape, 1 if random_operands else 0, stream or None, ctypes.byref(t)),
            "xc_mfma_rate")

@@ -152,7 +152,7 @@ def test_measurement_aids_reject_bad_arguments():
     lib = xcp.load_library()
     t = ctypes.c_double(-1.0)
     assert lib.xc_mfma_rate(0, 1, None, None) == xcp.XC_ERR_INVALID_ARG
-    assert lib.xc_mfma_rate(2, 1, None, ctypes.byref(t)) == xcp.XC_ERR_INVALID_ARG
+    assert lib.xc_mfma_rate(5, 1, None, ctypes.byref(t)) == xcp.XC_ERR_INVALID_ARG
     assert lib.xc_mfma_rate(-1, 0, None, ctypes.byref(t)) == xcp.XC_ERR_INVALID_ARG
     assert lib.xc_lds_dma_rate(128, None, None) == xcp.XC_ERR_INVALID_ARG
     assert lib.xc_lds_dma_rate(96, None, ctypes.byref(t)) == xcp.XC_ERR_INVALID_ARG

@@ -1,6 +1,8 @@
 """The measurement aids the benchmark reports next to the roofline: the
 register-only MFMA rate (positive, below the chip's dense bf16 peak, no
-slower on zero operands than on random ones) and the global -> LDS request
+slower on zero operands than on random ones), the MFMA rate under the
+attention loop's instruction mix (no faster than the register-only loop, the
+combined mix no faster than either part), and the global -> LDS request
 stream rate (positive, below what 256 CUs can take in)."""
 import pytest
 
@@ -23,6 +25,20 @@ def test_mfma_rate_is_plausible(shape):
     assert 100.0 < rnd <= 1.05 * PEAK_BF16_TFLOPS
     assert 100.0 < zero <= 1.05 * PEAK_BF16_TFLOPS
     assert zero >= 0.9 * rnd
+
+
+def test_attention_mix_rates_are_plausible():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2604_20289_amd import xcache as xcp
+    stream = torch.cuda.current_stream().cuda_stream
+    print("[mfma-mix] register-only 32x32x16, then + LDS reads, + softmax VALU, both", flush=True)
+    base = xcp.xc_mfma_rate(0, True, stream)
+    lds, valu, both = (xcp.xc_mfma_rate(s, True, stream) for s in (2, 3, 4))
+    print(f"[mfma-mix] {base:.0f} / {lds:.0f} / {valu:.0f} / {both:.0f} TFLOP/s", flush=True)
+    for r in (lds, valu, both):
+        assert 100.0 < r <= 1.05 * base
+    assert both <= 1.05 * min(lds, valu)
 
 
 @pytest.mark.parametrize("row_bytes", [64, 128, 256])
