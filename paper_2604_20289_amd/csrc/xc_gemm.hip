@@ -749,7 +749,10 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_wide(const bf16* __restrict_
   // caches), are requested two steps ahead.  Step k requests A(k+1) and then
   // W(k+2) (their slots were released by the barrier that ended step k-1),
   // multiplies stage k, and waits for everything but the W(k+2) requests
-  // (vmcnt counts in issue order).
+  // (vmcnt counts in issue order).  The barrier's workgroup release fence
+  // then also waits for those on this chip; a barrier without the fence,
+  // which leaves them in flight, measured the same (they land within a
+  // step), so the plain __syncthreads stays.
 #define XC_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt((0x3f70) | ((n) & 15) | (((n) >> 4) << 14))
   constexpr int WREQ = BN / 64;
   issue_w(0, 0);

@@ -210,6 +210,49 @@ def test_bf16_wide_skip_path(width, gate):
         ls.close()
 
 
+# Hidden sizes that are no multiple of 256 put the QKV projection (and the
+# cross-attention q and condition key / value projections) on the
+# two-workgroup GEMM and its QKV epilogue, whose tile height (64 * MT rows)
+# the library picks from the tile count on 256 CUs: N = 3C = 1152 at L = 300
+# takes MT = 2; N = 1920 (C = 640, 5 heads of 128) takes MT = 3 at L = 5000
+# (its per-lane sums of squares are padded from 48 to 64 for the
+# reduce-scatter) and MT = 4 at L = 7000.
+BF_TWO_WG = {
+    "h384-d64-L300-rope-cross": synth.with_model(synth.Workload(
+        "bf16-2wg-3blk-h384-d64-L300",
+        synth.ModelShape(3, 384, 6, 64, 768, 256, 16, synth.BF16, 4, 3, (synth.ViewGroup(2, 3, 5, 10),)),
+        synth.GateParams(), synth.StreamParams(4, 0.999, 0.02)), rope=1, cond_len=40),
+    "h384-d128-L300": synth.Workload(
+        "bf16-2wg-3blk-h384-d128-L300",
+        synth.ModelShape(3, 384, 3, 128, 768, 256, 16, synth.BF16, 4, 3, (synth.ViewGroup(2, 3, 5, 10),)),
+        synth.GateParams(), synth.StreamParams(4, 0.999, 0.02)),
+    "h640-d128-L5000-mt3": synth.Workload(
+        "bf16-2wg-1blk-h640-d128-L5000",
+        synth.ModelShape(1, 640, 5, 128, 1280, 256, 16, synth.BF16, 2, 2, (synth.ViewGroup(2, 1, 50, 50),)),
+        synth.GateParams(), synth.StreamParams(2, 0.999, 0.02)),
+    "h640-d128-L7000-mt4": synth.with_model(synth.Workload(
+        "bf16-2wg-1blk-h640-d128-L7000",
+        synth.ModelShape(1, 640, 5, 128, 1280, 256, 16, synth.BF16, 2, 2, (synth.ViewGroup(2, 1, 50, 70),)),
+        synth.GateParams(), synth.StreamParams(2, 0.999, 0.02)), rope=1),
+}
+
+
+@pytest.mark.parametrize("name", list(BF_TWO_WG))
+def test_bf16_two_workgroup_qkv_epilogue(name):
+    """The two-workgroup kernel's QKV epilogue (per-head RMSNorm, rotation, q /
+    K / V^T cache stores) at every tile height, head_dim 64 and 128, against
+    the oracle: pass outputs, residuals, r_hat and the key / value caches."""
+    w = BF_TWO_WG[name]
+    ls = _ls(w, compute=np.float32)
+    try:
+        st = ls.run(w.stream.n_chunks, tol_rel_l2=TOLBF)
+        print(f"[parity] {w.name}: skips={st['skips']} r_hat checked={ls.residuals_checked} "
+              f"kv slots={ls.kv_slots_checked} worst={max(ls.worst.values()):.2e}", flush=True)
+        assert ls.kv_slots_checked > 0
+    finally:
+        ls.close()
+
+
 @pytest.mark.slow
 def test_cfg1_prefix_parity():
     """Single-camera bf16 configuration, first 4 chunks, Table-1 gate."""
