@@ -270,6 +270,8 @@ def cold_gate(w, m, eps_dev, actions, make_xc, torch, xcp, n_pass=8):
     out = {}
     for mode in ("in_stream", "cold"):
         xc = xcp.XCache(m1, wg.gate, make_xc.weights[: synth.block_numel(m1)], make_xc.stream)
+        if make_xc.cond is not None:
+            xc.set_condition(make_xc.cond)
         L, C = m1.tokens, m1.hidden
         x = torch.empty((L, C), dtype=torch.float32, device="cuda")
         y = torch.empty_like(x)
@@ -396,7 +398,7 @@ def main():
         if cond is not None:
             xc.set_condition(cond)
         return xc
-    make_xc.weights, make_xc.stream = weights, stream
+    make_xc.weights, make_xc.stream, make_xc.cond = weights, stream, cond
 
     if args.calib_copy_mib:
         n = args.calib_copy_mib * (1 << 20) // 4

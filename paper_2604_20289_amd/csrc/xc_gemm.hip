@@ -869,6 +869,23 @@ void launch_bf16(const void* A, const void* W, int M, int N, int K, const EpiArg
   gemm_bf16_kernel<MODE, MT, 2><<<grid, 256, 0, st>>>((const bf16*)A, (const bf16*)W, M, N, K, e, flag);
 }
 
+// Whether wide 256 x BN tiles beat the two-workgroup kernel for an M x N
+// product: a round's time taken in proportion to the tile area a CU works
+// through (two resident (64*MT) x 128 tiles share a CU), the wide kernel
+// 12% more efficient per flop (the multi-camera QKV product: 122.8 against
+// 137.5 us in one round-count class).  Small token counts leave most CUs
+// idle under wide tiles (768 tokens: 18 tiles of 256 x 256 for the QKV
+// product), where the smaller tiles win.
+bool wide_pays(int M, int N, int BN) {
+  const long long cus = cu_count();
+  const long long wt = (long long)((M + WBM - 1) / WBM) * (N / BN);
+  const double wide = (double)((wt + cus - 1) / cus) * WBM * BN / 1.12;
+  const int mt = pick_mt(M, N);
+  const long long t2 = (long long)((M + 64 * mt - 1) / (64 * mt)) * (N / 128);
+  const double two = (double)((t2 + 2 * cus - 1) / (2 * cus)) * (64.0 * mt * 128.0) * 2.0;
+  return wide <= two;
+}
+
 template <int MODE, int BN, int WMW>
 void launch_wide(const void* A, const void* W, int M, int N, int K, const EpiArgs& e, const int* flag,
                  hipStream_t st) {
@@ -891,12 +908,12 @@ void launch_mode(int dtype, const void* A, const void* W, int M, int N, int K, c
     // (at hidden 2048 it measured 445 vs 451 us for MLP down and 132 vs
     // 136 us for the output projection against 256 x 256 wide tiles).
     if constexpr (MODE == EPI_QKV || MODE == EPI_UP) {
-      if (N % 256 == 0 && K % WBK == 0 && (MODE != EPI_QKV || (e.H * e.D) % 256 == 0)) {
+      if (N % 256 == 0 && K % WBK == 0 && (MODE != EPI_QKV || (e.H * e.D) % 256 == 0) && wide_pays(M, N, 256)) {
         launch_wide<MODE, 256, 2>(A, W, M, N, K, e, flag, st);
         return;
       }
     } else {
-      if (N % 192 == 0 && K % WBK == 0) {
+      if (N % 192 == 0 && K % WBK == 0 && wide_pays(M, N, 192)) {
         launch_wide<MODE, 192, 4>(A, W, M, N, K, e, flag, st);
         return;
       }

@@ -253,6 +253,27 @@ def test_bf16_two_workgroup_qkv_epilogue(name):
         ls.close()
 
 
+# The wide kernel's QKV epilogue with head_dim 64 (one wave per head): wide
+# tiles serve the QKV product only where they fill the chip (the multi-camera
+# token count), so this case runs at L = 7020 with hidden 1536 in 24 heads,
+# one block, two chunks, rotary embedding.
+BF_WIDE_D64 = synth.with_model(synth.Workload(
+    "bf16-wide-1blk-h1536-d64-L7020",
+    synth.ModelShape(1, 1536, 24, 64, 6144, 256, 16, synth.BF16, 2, 2, (synth.ViewGroup(2, 1, 54, 65),)),
+    synth.GateParams(), synth.StreamParams(2, 0.999, 0.02)), rope=1)
+
+
+def test_bf16_wide_qkv_epilogue_head64():
+    w = BF_WIDE_D64
+    ls = _ls(w, compute=np.float32)
+    try:
+        ls.run(w.stream.n_chunks, tol_rel_l2=TOLBF)
+        print(f"[parity] {w.name}: kv slots={ls.kv_slots_checked} worst={max(ls.worst.values()):.2e}", flush=True)
+        assert ls.kv_slots_checked > 0
+    finally:
+        ls.close()
+
+
 @pytest.mark.slow
 def test_cfg1_prefix_parity():
     """Single-camera bf16 configuration, first 4 chunks, Table-1 gate."""
