@@ -906,7 +906,8 @@ void launch_mode(int dtype, const void* A, const void* W, int M, int N, int K, c
     // 32-deep stages, which this replaced; 256 x 256 tiles leave 168 tiles
     // for 256 CUs at hidden 1536).  Other widths: the two-workgroup kernel
     // (at hidden 2048 it measured 445 vs 451 us for MLP down and 132 vs
-    // 136 us for the output projection against 256 x 256 wide tiles).
+    // 136 us for the output projection against 256 x 256 wide tiles), and
+    // products whose wide tiles leave the chip underfilled (wide_pays).
     if constexpr (MODE == EPI_QKV || MODE == EPI_UP) {
       if (N % 256 == 0 && K % WBK == 0 && (MODE != EPI_QKV || (e.H * e.D) % 256 == 0) && wide_pays(M, N, 256)) {
         launch_wide<MODE, 256, 2>(A, W, M, N, K, e, flag, st);
