@@ -844,7 +844,9 @@ int cu_count() {
 }
 
 // Rows per M-tile for an M x N product: the tile height (64*MT) whose tile
-// count best fills whole rounds of resident workgroups (2 per CU).
+// count best fills whole rounds of resident workgroups (2 per CU); 64-row
+// tiles only where even 128-row tiles leave CUs without one (small
+// products, e.g. 768 tokens), since they move more operand bytes per flop.
 int pick_mt(int M, int N) {
   const int slots = 2 * cu_count();
   int best = 4;
@@ -858,6 +860,7 @@ int pick_mt(int M, int N) {
       best = mt;
     }
   }
+  if (best == 2 && (long long)((M + 127) / 128) * (N / 128) < cu_count()) best = 1;
   return best;
 }
 
@@ -922,7 +925,8 @@ void launch_mode(int dtype, const void* A, const void* W, int M, int N, int K, c
     switch (pick_mt(M, N)) {
       case 4: launch_bf16<MODE, 4>(A, W, M, N, K, e, flag, st); break;
       case 3: launch_bf16<MODE, 3>(A, W, M, N, K, e, flag, st); break;
-      default: launch_bf16<MODE, 2>(A, W, M, N, K, e, flag, st); break;
+      case 2: launch_bf16<MODE, 2>(A, W, M, N, K, e, flag, st); break;
+      default: launch_bf16<MODE, 1>(A, W, M, N, K, e, flag, st); break;
     }
   } else {
     dim3 grid((N + 63) / 64, (M + 63) / 64);

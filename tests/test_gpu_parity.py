@@ -214,9 +214,10 @@ def test_bf16_wide_skip_path(width, gate):
 # cross-attention q and condition key / value projections) on the
 # two-workgroup GEMM and its QKV epilogue, whose tile height (64 * MT rows)
 # the library picks from the tile count on 256 CUs: N = 3C = 1152 at L = 300
-# takes MT = 2; N = 1920 (C = 640, 5 heads of 128) takes MT = 3 at L = 5000
-# (its per-lane sums of squares are padded from 48 to 64 for the
-# reduce-scatter) and MT = 4 at L = 7000.
+# takes MT = 1 (its per-lane sums of squares padded from 16 to 32 for the
+# reduce-scatter); N = 1920 (C = 640, 5 heads of 128) takes MT = 3 at L = 5000
+# (48 padded to 64) and MT = 4 at L = 7000, where the output and MLP-down
+# products take MT = 2; hidden 2048 at L = 7020 puts those two on MT = 4.
 BF_TWO_WG = {
     "h384-d64-L300-rope-cross": synth.with_model(synth.Workload(
         "bf16-2wg-3blk-h384-d64-L300",
@@ -234,6 +235,11 @@ BF_TWO_WG = {
         "bf16-2wg-1blk-h640-d128-L7000",
         synth.ModelShape(1, 640, 5, 128, 1280, 256, 16, synth.BF16, 2, 2, (synth.ViewGroup(2, 1, 50, 70),)),
         synth.GateParams(), synth.StreamParams(2, 0.999, 0.02)), rope=1),
+    # the output and MLP-down products (N = 2048, no multiple of 192) on 256-row tiles
+    "h2048-d128-L7020-oproj-down-mt4": synth.Workload(
+        "bf16-2wg-1blk-h2048-d128-L7020",
+        synth.ModelShape(1, 2048, 16, 128, 2048, 256, 16, synth.BF16, 1, 2, (synth.ViewGroup(2, 1, 54, 65),)),
+        synth.GateParams(), synth.StreamParams(2, 0.999, 0.02)),
 }
 
 
