@@ -480,17 +480,19 @@ int resident_attention_groups() {
 
 // Key splits per item.  Estimated time in key-tile steps of one resident
 // workgroup: rounds * (tiles per unit + 4 for the unit's prologue and
-// epilogue) + 4 S items / (resident workgroups) for the merge, over S <= 4
-// with chunks of at least 4 tiles (fitted to measured split sweeps on the
-// multi-camera shapes); only split counts whose partials fit in cap_floats
-// workspace floats are considered (S = 1 needs none).
+// epilogue) + 4 S items / (resident workgroups) for the merge (fitted to
+// measured split sweeps on the multi-camera shapes, where it picks S = 3),
+// over S <= 16 with chunks of at least 4 tiles: few items over a long window
+// (768 tokens, 8 heads, 3072 keys: 24 items) take more splits; only split
+// counts whose partials fit in cap_floats workspace floats are considered
+// (S = 1 needs none).
 int attention_splits(int L, int Lk, int H, int D, size_t cap_floats) {
   const int items = H * ((L + kQT - 1) / kQT);
   const int NT = (Lk + 63) / 64;
   const int slots = resident_attention_groups();
   int best = 1;
   double best_cost = 1e300;
-  for (int s = 1; s <= 4 && (s == 1 || NT / s >= 4); ++s) {
+  for (int s = 1; s <= 16 && (s == 1 || NT / s >= 4); ++s) {
     if (s > 1 && (size_t)items * s * (size_t)piece_floats(D) > cap_floats) break;
     const long long units = (long long)items * s;
     const long long rounds = (units + slots - 1) / slots;
