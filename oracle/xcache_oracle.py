@@ -44,12 +44,14 @@ applied.
 Pins (see ``tests/test_oracle_*.py``): textbook spot values for the
 elementwise functions, brute-force attention on tiny inputs and its closed
 forms, hand-computed fingerprint indices and metric values, the gate truth
-table and EMA closed form, and whole-stream invariants (zero thresholds give
+table and EMA closed form, hand-worked multi-generation decision sequences
+(the threshold read before the EMA update, the action channel, the staleness
+reset on compute: ``tests/gate_sequences.py``), and whole-stream invariants (zero thresholds give
 zero skips and the uncached output, KV-update passes never skip, a skipped
 block adds exactly its cached residual, zero adaLN weights make every block
-the identity, an evicted chunk has no influence).  Beyond those invariants the
-cached path as a whole has no independent numeric reference in the paper:
-its multi-chunk outputs are "parity unpinned" except through them.
+the identity, an evicted chunk has no influence).  Beyond those invariants and
+sequences the cached path as a whole has no independent numeric reference in
+the paper: its multi-chunk outputs are "parity unpinned" except through them.
 """
 from __future__ import annotations
 
