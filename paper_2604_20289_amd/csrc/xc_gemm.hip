@@ -906,11 +906,13 @@ void launch_mode(int dtype, const void* A, const void* W, int M, int N, int K, c
     // the two-workgroup kernel); the output and MLP-down projections on
     // 256 x 192 (the same box in one call: 49.6 vs 51.3 us and 145.6 vs
     // 147.6 us in the full pass against a persistent 4-wave kernel with
-    // 32-deep stages, which this replaced; 256 x 256 tiles leave 168 tiles
-    // for 256 CUs at hidden 1536).  Other widths: the two-workgroup kernel
-    // (at hidden 2048 it measured 445 vs 451 us for MLP down and 132 vs
-    // 136 us for the output projection against 256 x 256 wide tiles), and
-    // products whose wide tiles leave the chip underfilled (wide_pays).
+    // 32-deep stages, which this replaced, and 49.8 vs 54.7 us and 146.1 vs
+    // 163.2 us against the two-workgroup kernel on 192 x 128 tiles; 256 x 256
+    // tiles leave 168 tiles for 256 CUs at hidden 1536).  Other widths: the
+    // two-workgroup kernel (at hidden 2048 it measured 445 vs 451 us for MLP
+    // down and 132 vs 136 us for the output projection against 256 x 256
+    // wide tiles), and products whose wide tiles leave the chip underfilled
+    // (wide_pays).
     if constexpr (MODE == EPI_QKV || MODE == EPI_UP) {
       if (N % 256 == 0 && K % WBK == 0 && (MODE != EPI_QKV || (e.H * e.D) % 256 == 0) && wide_pays(M, N, 256)) {
         launch_wide<MODE, 256, 2>(A, W, M, N, K, e, flag, st);
