@@ -115,6 +115,11 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_bf16_kernel(const bf16* _
   const int kc = rem / n_qt, qt = rem - kc * n_qt;
   const int k0 = (int)((long long)kc * NT / n_split), k1 = (int)((long long)(kc + 1) * NT / n_split);
   const int q0 = qt * kQT + wave * 32;
+  // Waves whose 32 queries all lie past L (in a ragged last query tile) have
+  // nothing to compute: they only stage their share of the K / V^T tiles, in
+  // a loop of their own with the same barriers (a branch inside the shared
+  // loop instead costs the other waves registers).
+  const bool live = __builtin_amdgcn_readfirstlane(q0) < L;
 
   // thread tid stages K rows key0 + KSTEP i and V^T rows dd0 + VSTEP i: one
   // per-thread offset each, the i-steps are wave-uniform (row_of_key maps
@@ -263,6 +268,19 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_bf16_kernel(const bf16* _
       store_k(1);
     }
     __syncthreads();
+    if (!live) {
+      __syncthreads();
+      for (int j = k0; j < k1; ++j) {
+        // the buffers iteration j of the compute loop refills
+        const int odd = (j - k0) & 1;
+        if (j + 2 < k1) load_k(j + 2);
+        if (j + 1 < k1) load_v(j + 1);
+        if (j + 2 < k1) store_k(odd);
+        if (j + 1 < k1) store_v(1 - odd);
+        __syncthreads();
+      }
+      return;
+    }
     f32x16 sa[2], sb[2];
     qk(sa, 0);
     if (k0 == NT - 1) mask(sa, k0);
