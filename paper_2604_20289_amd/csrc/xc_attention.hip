@@ -16,7 +16,7 @@
 //     ([d][keys]) so a lane's 8-key operand is one 16-byte LDS read, and the K
 //     tile rows are permuted in LDS so that the score registers of each lane
 //     are exactly the 8 consecutive keys the P operand needs (no shuffles);
-//   * K and V^T tiles are double-buffered in LDS (rows padded by 16 bytes);
+//   * K and V^T tiles are double-buffered in LDS, filled by LDS-DMA;
 //     scores are scaled into the log2 domain by one FMA and exponentiated
 //     with exp2; the softmax denominator sums the bf16 probabilities that the
 //     P.V product consumes (two per dot2 instruction); accumulation is float.
@@ -32,7 +32,6 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 // MFMA row R of a 32-key M-tile -> key offset within the 64-key tile.
 //   R = g*8 + hh*4 + r  ->  key = mt*32 + (g/2)*16 + hh*8 + (g%2)*4 + r
@@ -45,6 +44,14 @@ __device__ __forceinline__ int row_of_key(int key) {
   const int mt = key >> 5, k = key & 31;
   const int g = ((k >> 4) << 1) | ((k >> 2) & 1), hh = (k >> 3) & 1, r = k & 3;
   return mt * 32 + g * 8 + hh * 4 + r;
+}
+
+// vmcnt(0), the other counters left alone (gfx9 encoding)
+#define XC_WAIT_VMCNT0() __builtin_amdgcn_s_waitcnt(0x3f70)
+// one 16-byte chunk per lane, global -> LDS (lane l lands at byte 16 l of
+// the wave's 1 KB block)
+__device__ __forceinline__ void dma16(const char* src, bf16* lds_block) {
+  __builtin_amdgcn_global_load_lds(src, lds_block, 16, 0, 0);
 }
 
 constexpr int kXcds = 8;
@@ -91,18 +98,25 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_bf16_kernel(const bf16* _
                                                            const int* __restrict__ flag) {
   if (flag != nullptr && *flag) return;
   constexpr int KCH = D / 8;                // 16-byte chunks per key row
-  constexpr int NTH = 64 * kWaves;          // threads per workgroup
-  constexpr int KLD = 64 * KCH / NTH;       // K chunks staged per thread
-  constexpr int VLD = D * 8 / NTH;          // V^T chunks staged per thread
+  constexpr int KCG = KCH / 8;              // groups of 8 chunks per K row
+  constexpr int KB = 8 * KCG / kWaves;      // K DMA blocks per wave and tile
+  constexpr int VB = D / 8 / kWaves;        // V^T DMA blocks per wave and tile
+  static_assert(KB >= 1 && VB >= 1, "staging layout");
   constexpr int DT = D / 32;                // 32-row output tiles (head dims)
-  // LDS rows are padded by 16 bytes: the 32 rows a half-wave reads at one
-  // chunk position fall in distinct banks, and every fragment address is a
-  // per-lane base plus a compile-time offset.
-  constexpr int KR = D + 8;                 // K tile row stride (elements)
-  constexpr int VR = 64 + 8;                // V^T tile row stride (elements)
-  __shared__ __attribute__((aligned(16))) bf16 sK[2][64 * KR];
-  __shared__ __attribute__((aligned(16))) bf16 sV[2][D * VR];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // K and V^T tiles go global -> LDS by DMA (no register staging), in 1 KB
+  // blocks of 8 rows x 8 sixteen-byte chunks: row r, chunk c sits in block
+  // (r / 8, c / 8) at slot ((c % 8) ^ (r / 8 % 2)) * 8 + r % 8.  A DMA
+  // instruction fills one block (each lane fetches the chunk its slot holds:
+  // 128-byte row segments), the 16 rows a quarter-wave reads at one chunk
+  // fall in 16 distinct 16-byte bank groups without padding, and every
+  // fragment address is a per-lane base plus a compile-time offset.
+  // Four separate arrays: the compiler then tells a DMA into one buffer from
+  // fragment reads of the other and does not wait for the DMA before them
+  __shared__ __attribute__((aligned(1024))) bf16 sK0[64 * D];
+  __shared__ __attribute__((aligned(1024))) bf16 sK1[64 * D];
+  __shared__ __attribute__((aligned(1024))) bf16 sV0[D * 64];
+  __shared__ __attribute__((aligned(1024))) bf16 sV1[D * 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int hi = lane >> 5, lo = lane & 31;
   const int C = H * D;
   const int NT = (Lk + 63) / 64;
@@ -121,20 +135,24 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_bf16_kernel(const bf16* _
   // loop instead costs the other waves registers).
   const bool live = __builtin_amdgcn_readfirstlane(q0) < L;
 
-  // thread tid stages K rows key0 + KSTEP i and V^T rows dd0 + VSTEP i: one
-  // per-thread offset each, the i-steps are wave-uniform (row_of_key maps
-  // key + 32 i to its row + 32 i for key < 32)
-  constexpr int KSTEP = NTH / KCH;
-  constexpr int VSTEP = NTH / 8;
-  static_assert(KSTEP == 32 || KSTEP == 64, "staging layout");
-  const int key0 = tid / KCH, kc0 = tid % KCH;
-  const int kg0 = (key0 * D + kc0 * 8) * 2;
-  const int ks0 = row_of_key(key0) * KR + kc0 * 8;
-  const int dd0 = tid >> 3, vc0 = tid & 7;
-  const int vg0 = (dd0 * Lcap + vc0 * 8) * 2;
-  const int vs0 = dd0 * VR + vc0 * 8;
-  const int k_frag = lo * KR + hi * 8;   // + mt*32*KR + ks*16
-  const int v_frag = lo * VR + hi * 8;   // + dt*32*VR + kv*16
+  // 1 KB DMA blocks of 8 rows x 8 chunks; slot ((c % 8) ^ (rg & 1)) * 8 + r % 8
+  // for row r (row group rg = r / 8) and chunk c
+  int kg[KB], vg[VB];
+#pragma unroll
+  for (int i = 0; i < KB; ++i) {
+    const int B = wave + kWaves * i, rg = B / KCG, cg = B % KCG;
+    const int R = rg * 8 + (lane & 7), c = cg * 8 + ((lane >> 3) ^ (rg & 1));
+    kg[i] = (key_of_row(R >> 5, R & 31) * D + c * 8) * 2;
+  }
+#pragma unroll
+  for (int i = 0; i < VB; ++i) {
+    const int rg = wave + kWaves * i;
+    const int d = rg * 8 + (lane & 7), c = (lane >> 3) ^ (rg & 1);
+    vg[i] = (d * Lcap + c * 8) * 2;
+  }
+  const int sw = hi ^ ((lo >> 3) & 1);
+  const int k_frag = (lo >> 3) * KCG * 1024 + sw * 128 + (lo & 7) * 16;  // bytes
+  const int v_frag = (lo >> 3) * 1024 + sw * 128 + (lo & 7) * 16;        // bytes
   const float lazy = 8.0f / sl2;
 
   {
@@ -156,28 +174,17 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_bf16_kernel(const bf16* _
       for (int r = 0; r < 16; ++r) oacc[i][r] = 0.f;
     float m_run = -INFINITY, l_run = 0.f;
 
-    u32x4 rk[KLD], rv[VLD];
-    auto load_k = [&](int j) __attribute__((always_inline)) {
+    auto dma_k = [&](int j, int buf) __attribute__((always_inline)) {
+      const char* base = Kh + (long long)j * 64 * D * 2;
 #pragma unroll
-      for (int i = 0; i < KLD; ++i) {
-        const char* base = Kh + ((long long)j * 64 + i * KSTEP) * D * 2;
-        rk[i] = *reinterpret_cast<const u32x4*>(base + kg0);
-      }
+      for (int i = 0; i < KB; ++i)
+        dma16(base + kg[i], (buf ? sK1 : sK0) + (wave + kWaves * i) * 512);
     };
-    auto load_v = [&](int j) __attribute__((always_inline)) {
+    auto dma_v = [&](int j, int buf) __attribute__((always_inline)) {
+      const char* base = Vh + (long long)j * 64 * 2;
 #pragma unroll
-      for (int i = 0; i < VLD; ++i) {
-        const char* base = Vh + ((long long)i * VSTEP * Lcap + j * 64) * 2;
-        rv[i] = *reinterpret_cast<const u32x4*>(base + vg0);
-      }
-    };
-    auto store_k = [&](int buf) __attribute__((always_inline)) {
-#pragma unroll
-      for (int i = 0; i < KLD; ++i) *reinterpret_cast<u32x4*>(&sK[buf][ks0 + i * KSTEP * KR]) = rk[i];
-    };
-    auto store_v = [&](int buf) __attribute__((always_inline)) {
-#pragma unroll
-      for (int i = 0; i < VLD; ++i) *reinterpret_cast<u32x4*>(&sV[buf][vs0 + i * VSTEP * VR]) = rv[i];
+      for (int i = 0; i < VB; ++i)
+        dma16(base + vg[i], (buf ? sV1 : sV0) + (wave + kWaves * i) * 512);
     };
     auto qk = [&](f32x16* sacc, int buf) __attribute__((always_inline)) {
 #pragma unroll
@@ -188,7 +195,8 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_bf16_kernel(const bf16* _
       for (int ks = 0; ks < D / 16; ++ks)
 #pragma unroll
         for (int mt = 0; mt < 2; ++mt) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(&sK[buf][k_frag + mt * 32 * KR + ks * 16]);
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(reinterpret_cast<const char*>(buf ? sK1 : sK0) + k_frag +
+                                                            mt * 4 * KCG * 1024 + (ks >> 2) * 1024 + (ks & 3) * 256);
           sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], sacc[mt], 0, 0, 0);
         }
     };
@@ -238,7 +246,8 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_bf16_kernel(const bf16* _
       for (int kv = 0; kv < 4; ++kv)
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(&sV[buf][v_frag + dt * 32 * VR + kv * 16]);
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(reinterpret_cast<const char*>(buf ? sV1 : sV0) + v_frag +
+                                                            dt * 4096 + kv * 256);
           oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kv], oacc[dt], 0, 0, 0);
         }
     };
@@ -259,24 +268,19 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_bf16_kernel(const bf16* _
     };
 
     // prologue: K(k0), V(k0), K(k0+1) in LDS; S(k0) and its max
-    load_k(k0);
-    load_v(k0);
-    store_k(0);
-    store_v(0);
-    if (k0 + 1 < k1) {
-      load_k(k0 + 1);
-      store_k(1);
-    }
+    dma_k(k0, 0);
+    dma_v(k0, 0);
+    if (k0 + 1 < k1) dma_k(k0 + 1, 1);
+    XC_WAIT_VMCNT0();
     __syncthreads();
     if (!live) {
       __syncthreads();
       for (int j = k0; j < k1; ++j) {
         // the buffers iteration j of the compute loop refills
         const int odd = (j - k0) & 1;
-        if (j + 2 < k1) load_k(j + 2);
-        if (j + 1 < k1) load_v(j + 1);
-        if (j + 2 < k1) store_k(odd);
-        if (j + 1 < k1) store_v(1 - odd);
+        if (j + 2 < k1) dma_k(j + 2, odd);
+        if (j + 1 < k1) dma_v(j + 1, 1 - odd);
+        XC_WAIT_VMCNT0();
         __syncthreads();
       }
       return;
@@ -288,16 +292,18 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_bf16_kernel(const bf16* _
     __syncthreads();  // the first iteration refills K buffer 0, which S(k0) just read
 
     // Iteration j (local index jj = j - k0; scur = S(j), its max already in m_run):
+    //   the DMA refills K(j+2) -> K buffer vb_cur and V(j+1) -> V buffer kb_next
+    //   (both last read in iteration j - 1) are issued first and land during
     //   region 1: S(j+1) MFMAs from K buffer kb_next  ||  probabilities of S(j)
     //   region 2: PV(j) MFMAs from V buffer vb_cur     ||  max of S(j+1)
-    //   then the (rare) rescale and the refills K(j+2) -> vb_cur, V(j+1) -> kb_next.
+    //   then the (rare) rescale, the wait for this wave's DMA and the barrier.
     // The steady-state loop calls it with constant buffer arguments and no
     // mask: no branch inside.
     auto iter = [&](int j, f32x16* scur, f32x16* snext, int kb_next, int vb_cur, bool has_next, bool mask_next)
         __attribute__((always_inline)) {
       const bool more_k = j + 2 < k1;
-      if (more_k) load_k(j + 2);
-      if (has_next) load_v(j + 1);
+      if (more_k) dma_k(j + 2, vb_cur);
+      if (has_next) dma_v(j + 1, kb_next);
       if (has_next) qk(snext, kb_next);
       bf16x8 pb[4];
       probs(scur, pb);
@@ -306,8 +312,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_bf16_kernel(const bf16* _
         if (mask_next) mask(snext, j + 1);
         update_max(tile_max(snext));
       }
-      if (more_k) store_k(vb_cur);
-      if (has_next) store_v(kb_next);
+      XC_WAIT_VMCNT0();
       __syncthreads();
     };
     const int n = k1 - k0;
