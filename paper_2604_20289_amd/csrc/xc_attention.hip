@@ -535,8 +535,9 @@ size_t attention_workspace_floats(int L, int Lk, int H, int D) {
 }
 
 // bf16 requirements (checked by the caller): D in {64, 128}; Q has Mpad >=
-// roundup(L, 256) rows per head; the caches have Lcap >= roundup(Lk, 64) rows
-// whose keys past Lk hold finite values; ws holds ws_floats floats (the key
+// roundup(L, 256) rows per head; the caches have Lcap >= roundup(Lk, 64) rows,
+// Lcap a multiple of 8 (16-byte aligned V^T rows for the DMA), 16-byte
+// aligned bases, and keys past Lk that hold finite values; ws holds ws_floats floats (the key
 // split is limited to what fits: attention_workspace_floats(L, Lk, H, D)
 // floats allow the unconstrained choice).
 void launch_attention(int dtype, const void* q, const void* kc, const void* vt, void* o, float* ws, size_t ws_floats,
