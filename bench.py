@@ -55,7 +55,7 @@ PEAK_HBM_GBS = 8000.0
 # scaled by a 512 MiB copy-kernel calibration; valid only for the workload and
 # the kernel source they were taken on (sha1 prefix of the file).
 MEASURED_TRAFFIC = {
-    "attention": {"source": "paper_2604_20289_amd/csrc/xc_attention.hip", "sha1": "84f9e572c791a142",
+    "attention": {"source": "paper_2604_20289_amd/csrc/xc_attention.hip", "sha1": "ccad982ddaa23cb7",
                   "workload": "multi-camera-bf16-dit-20blk-h1536-L7020", "bytes": (358.8 + 88.5) * 1e6},
 }
 

@@ -135,8 +135,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void attn_bf16_kernel(const bf16* _
   // loop instead costs the other waves registers).
   const bool live = __builtin_amdgcn_readfirstlane(q0) < L;
 
-  // 1 KB DMA blocks of 8 rows x 8 chunks; slot ((c % 8) ^ (rg & 1)) * 8 + r % 8
-  // for row r (row group rg = r / 8) and chunk c
+  // source byte offsets (within a tile) of the blocks this wave fills: lane l
+  // lands at slot l, i.e. row 8 rg + l % 8 and chunk 8 cg + ((l / 8) ^ (rg & 1));
+  // LDS row R of a K tile holds key key_of_row(R / 32, R % 32)
   int kg[KB], vg[VB];
 #pragma unroll
   for (int i = 0; i < KB; ++i) {
